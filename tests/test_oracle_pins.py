@@ -1,0 +1,510 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test ties one part of the oracle to something other than itself: a
+worked example derived by hand from Equation 3 and Algorithm 2, closed forms
+and invariants of the compressor (contraction identities, error-feedback
+telescoping), brute-force bit packing, an exact rational average, the
+special case in which 0/1 Adam reduces to Adam (Equation 2, computed by an
+independent binary64 implementation), and the consensus of workers after a
+synchronisation.
+"""
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle as orc
+from oracle.brute_adam import adam_fp64
+
+F32 = np.float32
+U = 2.0 ** -24  # unit roundoff of binary32
+
+
+def rng(seed):
+    return np.random.default_rng(seed)
+
+
+# ---------------------------------------------------------------------------
+# Worked example (Equation 3 + Algorithm 2 + the sync lines of Algorithm 1),
+# derived by hand; every number below is exact in binary32.
+# ---------------------------------------------------------------------------
+
+def test_worked_example_compress_server_sync():
+    lay = orc.Layout.from_lengths([4])
+    a = np.array([3, -1, 0, -4], F32)
+    delta = np.zeros(4, F32)
+    words, scales = orc.ef_compress(lay, a, delta)
+    # |a|_1 by the tree: (3 + 1) + (0 + 4) = 8, s = 8 / 4 = 2
+    assert scales[0] == F32(2.0)
+    # signs +,-,+(zero),-  -> bits 1,0,1,0 LSB first -> 0b0101
+    assert int(words[0]) == 0x5
+    # new error a - s*sign = [1, 1, -2, -2]
+    np.testing.assert_array_equal(delta, np.array([1, 1, -2, -2], F32))
+
+    # server with W = 2: peer signs +,+,-,- (0b0011) with scale 1
+    words_w = np.array([[0x5], [0x3]], np.uint64)
+    scales_w = np.array([[2.0], [1.0]], F32)
+    srv_err = np.zeros(4, F32)
+    sw, ss, avg = orc.server(lay, words_w, scales_w, srv_err, want_avg=True)
+    # ([2,-2,2,-2] + [1,1,-1,-1]) / 2
+    np.testing.assert_array_equal(avg, np.array([1.5, -0.5, 0.5, -1.5], F32))
+    # tree (1.5 + 0.5) + (0.5 + 1.5) = 4, s = 1; signs +,-,+,- -> 0b0101
+    assert ss[0] == F32(1.0) and int(sw[0]) == 0x5
+    np.testing.assert_array_equal(srv_err, np.array([0.5, 0.5, -0.5, -0.5], F32))
+    ubar = orc.decompress(lay, sw, ss)
+    np.testing.assert_array_equal(ubar, np.array([1, -1, 1, -1], F32))
+
+    # sync with Gamma = 0.5, v = 4 (sqrt(4 + 1e-8) rounds to 2), anchor = 10
+    w = orc.Worker(lay, np.full(4, 10, F32))
+    w.v[:] = 4.0
+    w.gamma_sum = F32(0.5)
+    w.sync(sw, ss)
+    np.testing.assert_array_equal(w.m, np.array([2, -2, 2, -2], F32))
+    np.testing.assert_array_equal(w.x, np.array([9.5, 10.5, 9.5, 10.5], F32))
+    np.testing.assert_array_equal(w.anchor, w.x)
+    assert not w.u.any() and w.gamma_sum == 0
+
+
+# ---------------------------------------------------------------------------
+# The L1 tree
+# ---------------------------------------------------------------------------
+
+def test_tree_is_pairwise_in_index_order():
+    big = float(2 ** 24)
+    # pairwise: (1 + 1) + (1 + 2^24) = 2 + 2^24 (1 + 2^24 ties to even 2^24)
+    assert orc.tree_abs_sum(np.array([1, 1, 1, big], F32)) == F32(big + 2)
+    # left to right would give ((1 + 1) + 1) + 2^24 = 2^24 + 3 -> 2^24 + 4
+    assert F32(F32(F32(1 + 1) + 1) + F32(big)) == F32(big + 4)
+    # [2^24, 1, 1, 1]: (2^24 + 1) + (1 + 1) = 2^24 + 2
+    assert orc.tree_abs_sum(np.array([big, 1, 1, 1], F32)) == F32(big + 2)
+    # absolute values are summed
+    assert orc.tree_abs_sum(np.array([-3, 1, -0.0, -4], F32)) == F32(8)
+    # zero padding: n = 3 is the tree over [a0, a1, a2, 0]
+    assert orc.tree_abs_sum(np.array([big, 1, 1], F32)) == F32(big)   # (2^24+1)+(1+0)
+    assert orc.tree_abs_sum(np.array([1, 1, big], F32)) == F32(big + 2)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 7, 64, 100, 1000, 4096, 16383])
+def test_tree_error_bound(n):
+    """Pairwise summation: |T - sum| <= ceil(log2 n) * u * sum |a| (Higham)."""
+    a = rng(n).standard_normal(n).astype(F32) * F32(1e-3)
+    exact = math.fsum(abs(float(v)) for v in a)
+    t = float(orc.tree_abs_sum(a))
+    k = max(1, math.ceil(math.log2(n))) if n > 1 else 0
+    assert abs(t - exact) <= k * U * exact * 1.0001 + 1e-45
+
+
+# ---------------------------------------------------------------------------
+# Equation 3 on a chunk: closed forms and invariants
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n", [1, 2, 5, 64, 65, 1000, 2048])
+def test_compressor_identities(n):
+    r = rng(100 + n)
+    a = (r.standard_normal(n) * 1e-3).astype(F32)
+    s, bits = orc.compress_chunk(a)
+    sigma = np.where(bits == 1, 1.0, -1.0)
+    np.testing.assert_array_equal(bits, (a >= 0).astype(np.uint8))
+    l1 = math.fsum(abs(float(v)) for v in a)
+    # s = |a|_1 / n up to the tree's and the division's rounding
+    k = max(1, math.ceil(math.log2(n))) if n > 1 else 0
+    assert abs(float(s) - l1 / n) <= (k + 1) * U * (l1 / n) * 1.0001
+    # the new error delta' = a - s sigma, each entry rounded once
+    lay = orc.Layout.from_lengths([n])
+    delta = np.zeros(n, F32)
+    orc.ef_compress(lay, a, delta)
+    ad = a.astype(np.float64)
+    dd = delta.astype(np.float64)
+    # C[a] + delta' = a up to one rounding of delta'
+    assert np.all(np.abs(sigma * float(s) + dd - ad) <= U * np.abs(dd) + 1e-45)
+    # <sigma, delta'> = |a|_1 - n s = 0 up to rounding
+    assert abs(math.fsum(sigma * dd)) <= (k + 4) * U * l1
+    # |delta'|^2 = |a|^2 - |a|_1^2 / n  (the contraction of Assumption 6)
+    lhs = math.fsum(dd * dd)
+    rhs = math.fsum(ad * ad) - l1 * l1 / n
+    assert abs(lhs - rhs) <= 8 * (k + 4) * U * math.fsum(ad * ad) + 1e-30
+    if n == 1:
+        assert delta[0] == 0
+
+
+@pytest.mark.parametrize("n", [1, 3, 64, 100, 2048])
+def test_constant_magnitude_is_lossless(n):
+    r = rng(7 * n)
+    c = F32(2.0 ** -13)
+    a = np.where(r.random(n) < 0.5, -c, c).astype(F32)
+    lay = orc.Layout.from_lengths([n])
+    delta = np.zeros(n, F32)
+    words, scales = orc.ef_compress(lay, a, delta)
+    assert scales[0] == c
+    assert not delta.any()
+    np.testing.assert_array_equal(orc.decompress(lay, words, scales), a)
+
+
+def test_sign_of_zero_is_plus():
+    s, bits = orc.compress_chunk(np.array([0.0, -0.0, -1.0, 1.0], F32))
+    assert list(bits) == [1, 1, 0, 1]
+    assert s == F32(0.5)
+
+
+def test_single_chunk_is_equation3():
+    """C = d on one segment: one magnitude |a|_1/d for the whole vector."""
+    d = 3000
+    a = (rng(5).standard_normal(d) * 0.01).astype(F32)
+    lay = orc.Layout.from_segments([0, d], d)
+    assert lay.nchunks == 1
+    delta = np.zeros(d, F32)
+    words, scales = orc.ef_compress(lay, a, delta)
+    l1 = math.fsum(abs(float(v)) for v in a)
+    assert abs(float(scales[0]) - l1 / d) <= 13 * U * l1 / d
+    out = orc.decompress(lay, words, scales)
+    np.testing.assert_array_equal(np.sign(out), np.where(a >= 0, 1, -1))
+
+
+def test_error_feedback_telescopes():
+    """sum_k C[z_k + delta_k] = sum_k z_k - delta_K with delta_0 = 0."""
+    lay = orc.Layout.from_segments([0, 500, 1300], 256)
+    r = rng(11)
+    delta = np.zeros(lay.n, F32)
+    sent = np.zeros(lay.n)
+    total = np.zeros(lay.n)
+    bound = np.zeros(lay.n)
+    for _ in range(12):
+        z = (r.standard_normal(lay.n) * 1e-2).astype(F32)
+        before = delta.astype(np.float64).copy()
+        words, scales = orc.ef_compress(lay, z, delta)
+        c = orc.decompress(lay, words, scales).astype(np.float64)
+        sent += c
+        total += z
+        # roundings of a = z + delta and of delta' = a -+ s
+        bound += U * (np.abs(z.astype(np.float64) + before) + np.abs(delta.astype(np.float64)))
+    resid = sent - (total - delta.astype(np.float64))
+    assert np.all(np.abs(resid) <= 2 * bound + 1e-30)
+
+
+# ---------------------------------------------------------------------------
+# Packing
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n", [1, 31, 32, 63, 64, 65, 128, 200])
+def test_pack_layout_brute_force(n):
+    bits = (rng(n).random(n) < 0.5).astype(np.uint8)
+    words = orc.pack_chunk(bits)
+    assert len(words) == (n + 63) // 64
+    expect = [0] * len(words)
+    for j in range(n):
+        if bits[j]:
+            expect[j // 64] |= 1 << (j % 64)
+    assert [int(w) for w in words] == expect
+    np.testing.assert_array_equal(orc.unpack_chunk(words, n), bits)
+    if n % 64:
+        assert int(words[-1]) >> (n % 64) == 0  # pad bits are zero
+
+
+def test_pack_bit_positions():
+    bits = np.zeros(130, np.uint8)
+    bits[0] = bits[63] = bits[64] = bits[129] = 1
+    w = orc.pack_chunk(bits)
+    assert [int(x) for x in w] == [1 | (1 << 63), 1, 2]
+
+
+def test_chunk_table_never_crosses_segments():
+    seg = [0, 100, 100 + 4096, 100 + 4096 + 8, 20000]
+    lay = orc.Layout.from_segments(seg, 1024)
+    ends = set(seg[1:])
+    pos = 0
+    words = 0
+    for c in range(lay.nchunks):
+        assert lay.cstart[c] == pos and 1 <= lay.clen[c] <= 1024
+        assert lay.cword[c] == words
+        pos += lay.clen[c]
+        words += (lay.clen[c] + 63) // 64
+        # a chunk ends at a segment end or after exactly 1024 elements
+        assert pos in ends or lay.clen[c] == 1024
+        assert not any(lay.cstart[c] < e < pos for e in ends)
+    assert pos == seg[-1] and lay.nwords == words
+    assert lay.nchunks == 1 + 4 + 1 + 16  # 100 | 4096 | 8 | 15796
+
+
+# ---------------------------------------------------------------------------
+# Server average: exact rational reference
+# ---------------------------------------------------------------------------
+
+def rn32(q: Fraction) -> np.float32:
+    """Round a rational to the nearest binary32, ties to even (exact)."""
+    f = np.float32(float(q))
+    best = f
+    for cand in (np.nextafter(f, F32(-np.inf)), f, np.nextafter(f, F32(np.inf))):
+        dc, db = abs(Fraction(float(cand)) - q), abs(Fraction(float(best)) - q)
+        if dc < db or (dc == db and (cand.view(np.uint32) & 1) == 0):
+            best = cand
+    return best
+
+
+@pytest.mark.parametrize("W", [1, 2, 3, 4, 5, 8, 16])
+def test_server_average_is_exact_rounding(W):
+    n = 200
+    r = rng(1000 + W)
+    lay = orc.Layout.from_lengths([n])
+    words_w = np.stack([orc.pack_chunk((r.random(n) < 0.5).astype(np.uint8)) for _ in range(W)])
+    scales_w = (r.uniform(0.5, 1.5, size=(W, 1)) * 3e-5).astype(F32)
+    srv_err = np.zeros(n, F32)
+    _, _, avg = orc.server(lay, words_w, scales_w, srv_err, want_avg=True)
+    for j in range(n):
+        tot = Fraction(0)
+        for w in range(W):
+            b = (int(words_w[w, j // 64]) >> (j % 64)) & 1
+            tot += Fraction(float(scales_w[w, 0])) * (1 if b else -1)
+        assert avg[j] == rn32(tot / W), (j, W)
+
+
+def test_server_single_worker_and_equal_signs():
+    n = 128
+    r = rng(3)
+    lay = orc.Layout.from_lengths([n])
+    bits = (r.random(n) < 0.5).astype(np.uint8)
+    own = orc.pack_chunk(bits)
+    s = F32(3.0e-6)
+    # W = 1: the average is the own decompressed value; recompressing a
+    # constant-magnitude chunk of power-of-two length loses nothing
+    srv_err = np.zeros(n, F32)
+    sw, ss, avg = orc.server(lay, own[None], np.array([[s]], F32), srv_err, want_avg=True)
+    np.testing.assert_array_equal(avg, np.where(bits == 1, s, -s).astype(F32))
+    assert ss[0] == s and int(sw[0]) == int(own[0]) and int(sw[1]) == int(own[1])
+    assert not srv_err.any()
+    # all workers agree on the signs: avg = +-(sum S_w) / W
+    W = 4
+    sc = np.array([[1e-6], [2e-6], [3e-6], [1.5e-6]], F32)
+    _, _, avg = orc.server(lay, np.repeat(own[None], W, 0), sc, np.zeros(n, F32), want_avg=True)
+    mag = rn32(sum(Fraction(float(v)) for v in sc[:, 0]) / W)
+    np.testing.assert_array_equal(avg, np.where(bits == 1, mag, -mag).astype(F32))
+
+
+def test_server_flags_inexact_sum():
+    lay = orc.Layout.from_lengths([64])
+    words_w = np.array([[0], [0xFFFFFFFFFFFFFFFF]], np.uint64)
+    scales_w = np.array([[1.0], [2.0 ** -60]], F32)
+    with pytest.raises(orc.OracleError):
+        orc.server(lay, words_w, scales_w, np.zeros(64, F32))
+
+
+def test_server_error_feedback_telescopes():
+    """Server half: sum_k sbar_k sigma_k = sum_k avg_k - serr_K."""
+    lay = orc.Layout.from_segments([0, 300, 812], 128)
+    r = rng(21)
+    W = 4
+    srv_err = np.zeros(lay.n, F32)
+    sent = np.zeros(lay.n)
+    total = np.zeros(lay.n)
+    bound = np.zeros(lay.n)
+    for _ in range(8):
+        words_w = r.integers(0, 2 ** 63, size=(W, lay.nwords), dtype=np.uint64)
+        scales_w = (r.uniform(0.5, 1.5, size=(W, lay.nchunks)) * 1e-5).astype(F32)
+        before = srv_err.astype(np.float64).copy()
+        sw, ss, avg = orc.server(lay, words_w, scales_w, srv_err, want_avg=True)
+        sent += orc.decompress(lay, sw, ss)
+        total += avg
+        bound += U * (np.abs(avg.astype(np.float64) + before) + np.abs(srv_err.astype(np.float64)))
+    resid = sent - (total - srv_err.astype(np.float64))
+    assert np.all(np.abs(resid) <= 2 * bound + 1e-30)
+
+
+def test_server_ignores_pad_bits():
+    lay = orc.Layout.from_segments([0, 100], 100)
+    r = rng(4)
+    W = 3
+    words = r.integers(0, 2 ** 63, size=(W, lay.nwords), dtype=np.uint64)
+    scales = (r.uniform(0.5, 1.5, size=(W, 1)) * 1e-4).astype(F32)
+    e1 = np.zeros(100, F32)
+    a1 = orc.server(lay, words, scales, e1, want_avg=True)
+    masked = words.copy()
+    masked[:, 1] &= np.uint64((1 << 36) - 1)
+    e2 = np.zeros(100, F32)
+    a2 = orc.server(lay, masked, scales, e2, want_avg=True)
+    np.testing.assert_array_equal(a1[2], a2[2])
+    np.testing.assert_array_equal(e1, e2)
+    assert int(a1[0][1]) >> 36 == 0
+
+
+# ---------------------------------------------------------------------------
+# Algorithm 1 special cases
+# ---------------------------------------------------------------------------
+
+def _grads(n, steps, seed, sigma=1e-3):
+    r = rng(seed)
+    return [(r.standard_normal(n) * sigma).astype(F32) for _ in range(steps)]
+
+
+def test_reduces_to_adam_when_every_step_syncs():
+    """T_u = T_v = all steps, W = 1, compression off  ==>  Adam (Equation 2)."""
+    n, T = 4096, 20
+    x0 = (rng(1).standard_normal(n) * 0.02).astype(F32)
+    grads = _grads(n, T, 2)
+    gammas = [F32(1e-4)] * T
+    ref = adam_fp64(x0, grads, gammas)
+    w = orc.Worker(orc.Layout.from_segments([0, n], 1024), x0)
+    for t in range(T):
+        w.step(gammas[t], grads[t], sync=True, var=True, compress=False)
+        x, m, v = ref[t]
+        np.testing.assert_allclose(w.v, v, rtol=2e-6, atol=0)
+        # momentum entries near zero come from cancellation: the floor is
+        # relative to the tensor's magnitude (binary32 rounding of the terms)
+        np.testing.assert_allclose(w.m, m, rtol=1e-6, atol=1e-6 * np.abs(m).max())
+        np.testing.assert_allclose(w.x, x, rtol=1e-6, atol=1e-7)
+        np.testing.assert_array_equal(w.anchor, w.x)
+        assert not w.u.any() and w.gamma_sum == 0
+
+
+def test_reduces_to_adam_without_sync():
+    """T_u empty, T_v = all steps: the local lines are Adam on the model."""
+    n, T = 2048, 15
+    x0 = (rng(3).standard_normal(n) * 0.02).astype(F32)
+    grads = _grads(n, T, 4)
+    gammas = [F32(1e-4 * (1 + t)) for t in range(T)]
+    ref = adam_fp64(x0, grads, gammas)
+    w = orc.Worker(orc.Layout.from_segments([0, n], 512), x0)
+    for t in range(T):
+        w.step(gammas[t], grads[t], sync=False, var=True)
+        x, m, v = ref[t]
+        np.testing.assert_allclose(w.m, m, rtol=1e-6, atol=1e-6 * np.abs(m).max())
+        np.testing.assert_allclose(w.v, v, rtol=2e-6, atol=0)
+        np.testing.assert_allclose(w.x, x, rtol=1e-6, atol=1e-7)
+    # the anchor never moves without a sync; u holds sum gamma m
+    np.testing.assert_array_equal(w.anchor, x0)
+    u_ref = sum(float(g) * ref[t][1] for t, g in enumerate(gammas))
+    np.testing.assert_allclose(w.u, u_ref, rtol=1e-5, atol=1e-6 * np.abs(u_ref).max())
+    assert w.gamma_sum == pytest.approx(sum(float(g) for g in gammas), rel=1e-6)
+
+
+def test_unit_chunks_make_compression_lossless():
+    """Chunk length 1: every scale is |a|, so compressing loses nothing and the
+    run equals the uncompressed run bit for bit (W = 1)."""
+    n, T = 512, 12
+    x0 = (rng(5).standard_normal(n) * 0.02).astype(F32)
+    grads = _grads(n, T, 6)
+    lay1 = orc.Layout.from_segments([0, n], 1)
+    a = orc.Worker(lay1, x0)
+    b = orc.Worker(lay1, x0)
+    sync = [t % 3 == 2 for t in range(T)]
+    var = [t < 4 for t in range(T)]
+    for t in range(T):
+        a.step(F32(1e-4), grads[t], sync[t], var[t], compress=True)
+        b.step(F32(1e-4), grads[t], sync[t], var[t], compress=False)
+        for k in ("x", "m", "v", "u", "anchor"):
+            np.testing.assert_array_equal(getattr(a, k), getattr(b, k))
+        assert not a.err.any() and not a.srv_err.any()
+
+
+def test_literal_momentum_index_freezes_momentum():
+    """Literal reading of the model/buffer lines (old momentum) with a sync at
+    every step: u = gamma m_t, ubar = u, m_{t+1} = ubar / gamma = m_t = 0."""
+    n, T = 256, 6
+    x0 = (rng(8).standard_normal(n) * 0.02).astype(F32)
+    grads = _grads(n, T, 9)
+    lay = orc.Layout.from_segments([0, n], 64)
+    lit = orc.Worker(lay, x0, literal_momentum=True)
+    fresh = orc.Worker(lay, x0)
+    for t in range(T):
+        lit.step(F32(1e-4), grads[t], True, True, compress=False)
+        fresh.step(F32(1e-4), grads[t], True, True, compress=False)
+        assert not lit.m.any()
+        np.testing.assert_array_equal(lit.x, x0)
+    assert np.abs(fresh.x - x0).max() > 0
+
+
+def test_variance_frozen_outside_tv_and_bounded():
+    """v is bit-unchanged at t not in T_v, and v <= (1 - b2^k) max gbar^2 after
+    k updates (the bound behind the paper's variance lemma)."""
+    n, T = 1000, 12
+    x0 = np.zeros(n, F32)
+    grads = _grads(n, T, 10)
+    gbars = _grads(n, T, 11)
+    tv = {0, 1, 3, 7}
+    w = orc.Worker(orc.Layout.from_segments([0, n], 256), x0)
+    k = 0
+    gmax = 0.0
+    for t in range(T):
+        before = w.v.copy()
+        w.step(F32(1e-4), grads[t], t % 2 == 1, t in tv, gbar=gbars[t], peer_words=None)
+        if t in tv:
+            k += 1
+            gmax = max(gmax, float(np.max(gbars[t].astype(np.float64) ** 2)))
+        else:
+            np.testing.assert_array_equal(w.v.view(np.uint32), before.view(np.uint32))
+        b2 = float(F32(0.999))
+        assert np.all(w.v <= (1 - b2 ** k) * gmax * (1 + 1e-5))
+
+
+def test_sync_with_frozen_variance_is_linear():
+    """With v frozen, W = 1 and no compression, the synced model equals the
+    model the local lines would have produced (x_{t'} - u / sqrt(v + eps)), and
+    the momentum becomes the Gamma-weighted mean of the interval's momenta."""
+    n = 1024
+    x0 = (rng(12).standard_normal(n) * 0.02).astype(F32)
+    grads = _grads(n, 6, 13)
+    gammas = [F32(1e-4), F32(2e-4), F32(3e-4), F32(1.5e-4), F32(1e-4), F32(5e-5)]
+    lay = orc.Layout.from_segments([0, n], 256)
+    w = orc.Worker(lay, x0)
+    w.step(gammas[0], grads[0], sync=True, var=True, compress=False)   # v set, synced
+    anchor = w.x.copy()
+    local = orc.Worker(lay, x0)
+    local.x[:], local.m[:], local.v[:] = w.x, w.m, w.v
+    moms, gs = [], []
+    for t in range(1, 6):
+        last = t == 5
+        local.step(gammas[t], grads[t], sync=False, var=False)
+        moms.append(local.m.astype(np.float64).copy())
+        gs.append(float(gammas[t]))
+        w.step(gammas[t], grads[t], sync=last, var=False, compress=False)
+    np.testing.assert_array_equal(w.anchor, w.x)
+    assert not np.array_equal(w.x, anchor)
+    # model: synced == local, up to the local path's per-step roundings
+    scale = np.abs(local.x.astype(np.float64) - anchor).max()
+    assert np.abs(w.x.astype(np.float64) - local.x).max() <= 1e-5 * scale + 4 * U * 0.1
+    # momentum: ubar / Gamma == sum gamma_h m_h / sum gamma_h
+    mean = sum(g * m for g, m in zip(gs, moms)) / sum(gs)
+    np.testing.assert_allclose(w.m, mean, rtol=1e-5, atol=1e-6 * np.abs(mean).max())
+
+
+def test_workers_reach_consensus_and_single_gpu_formulation_matches():
+    """W real workers with their own gradients and a real server: after every
+    sync all workers hold bit-identical x and m (the paper's consensus at sync
+    steps).  Worker 0 run alone, fed the other workers' packed buffers as
+    inputs, follows the identical trajectory."""
+    W, T = 4, 9
+    seg = [0, 700, 1024 + 700]
+    lay = orc.Layout.from_segments(seg, 256)
+    x0 = (rng(14).standard_normal(lay.n) * 0.02).astype(F32)
+    workers = [orc.Worker(lay, x0) for _ in range(W)]
+    solo = orc.Worker(lay, x0)
+    server_err = np.zeros(lay.n, F32)
+    grads = [_grads(lay.n, T, 100 + w) for w in range(W)]
+    gbars = _grads(lay.n, T, 99)
+    tu = {1, 3, 4, 8}
+    tv = {0, 1, 2, 5}
+    for t in range(T):
+        gamma = F32(1e-4 * (1 + 0.1 * t))
+        for w in range(W):
+            workers[w].half_step(gamma, grads[w][t])
+        if t in tu:
+            sent = [wk.compress() for wk in workers]
+            words_w = np.stack([s[0] for s in sent])
+            scales_w = np.stack([s[1] for s in sent])
+            sw, ss, _ = orc.server(lay, words_w, scales_w, server_err)
+            for wk in workers:
+                wk.sync(sw, ss)
+            out = solo.step(gamma, grads[0][t], True, t in tv, gbar=gbars[t],
+                            peer_words=words_w[1:], peer_scales=scales_w[1:])
+            assert np.array_equal(out["own_words"], words_w[0])
+            np.testing.assert_array_equal(out["srv_words"], sw)
+            for wk in workers[1:]:
+                np.testing.assert_array_equal(wk.x, workers[0].x)
+                np.testing.assert_array_equal(wk.m, workers[0].m)
+        else:
+            solo.step(gamma, grads[0][t], False, t in tv, gbar=gbars[t])
+        if t in tv:
+            for wk in workers:
+                wk.variance(gbars[t])
+        for k in ("x", "m", "v", "u", "err", "anchor"):
+            np.testing.assert_array_equal(getattr(solo, k), getattr(workers[0], k))
+        np.testing.assert_array_equal(solo.srv_err, server_err)
