@@ -1,0 +1,217 @@
+"""Benchmark of the 0/1 Adam hot path on one MI355X.
+
+Workload: the GPT-2-1.5B-shaped shard (d = 1,557,611,200 binary32 params in
+580 segments, chunk 16384, W = 128 workers whose packed sign buffers sit in
+HBM, the single server over the whole shard).  One bench step is two
+optimizer steps that together run every kernel of the path once:
+  step 2k   (local, variance update):  K_local+var         (zo_local_step)
+  step 2k+1 (sync, variance update):   K_sync1             (zo_compress_pack_ef)
+                                       K_srv, W = 128      (zo_unpack_average)
+                                       K_recon+var         (zo_sync_update)
+Inputs (gradient, averaged gradient, peers' packed signs and scales) are
+generated once on the device before timing and stay resident in HBM.
+`value` is optimizer-step parameter updates per second (2 d per bench step).
+
+Per-kernel durations come from HIP events recorded on the stream the kernels
+run on; the dominant kernel's algorithmic bytes per launch over its average
+duration gives the roofline line.  The CPU baseline times the oracle on a
+bounded contiguous slice of the same shard (rank 0, N = 1 only).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes(d, nchunks, nwords, W):
+    """Bytes each kernel must move per launch: every state read once and
+    written once, packed words and per-chunk scales included."""
+    pk = 8 * nwords
+    sc = 4 * nchunks
+    return {
+        # reads g, m, x, v, u, gbar; writes m, x, u, v
+        "local+var": 40 * d,
+        # reads g, m, u, err; writes err, own packed words, own scales
+        "sync1": 20 * d + pk + sc,
+        # reads W packed buffers + W scale rows + server error;
+        # writes server error, server packed words, server scales
+        "srv": W * (pk + sc) + 8 * d + pk + sc,
+        # reads server words + scales, v, anchor, gbar; writes m, x, anchor, u, v
+        "recon+var": pk + sc + 32 * d,
+    }
+
+
+def cpu_baseline(wl, sample_chunks):
+    """Time the oracle on the first `sample_chunks` chunks of the shard: one
+    local step with variance update and one sync step with variance update,
+    W = 128 (input generation excluded)."""
+    import numpy as np
+    import oracle as orc
+    import synth
+    from synth import configs as C
+    full = orc.Layout.from_segments(wl.seg_off, wl.chunk)
+    nch = min(sample_chunks, full.nchunks)
+    lay = orc.Layout.from_lengths(full.clen[:nch])
+    n = lay.n
+    ks = C.ksigma(wl.sigma_g)
+    x0 = synth.normal_host(n, 0, synth.key(0, C.STREAM_X, 0), C.ksigma(wl.sigma_x))
+    g = synth.normal_host(n, 0, synth.key(0, C.STREAM_G, 0), ks, wl.outlier_per_mille,
+                          wl.outlier_factor)
+    gb = synth.normal_host(n, 0, synth.key(0, C.STREAM_GBAR, 0), ks, wl.outlier_per_mille,
+                           wl.outlier_factor)
+    W = wl.world
+    base = np.float32(2 * 1e-4 * 0.18 * wl.sigma_g)
+    pw = np.stack([synth.bits_host(lay.nwords, 0, synth.key(w, C.STREAM_BITS, 1))
+                   for w in range(1, W)])
+    ps = np.stack([synth.scales_host(nch, 0, synth.key(w, C.STREAM_SCALES, 1), base)
+                   for w in range(1, W)])
+    worker = orc.Worker(lay, x0, wl.beta1, wl.beta2, wl.eps)
+    t0 = time.perf_counter()
+    worker.step(np.float32(1e-4), g, False, True, gbar=gb)
+    worker.step(np.float32(1e-4), g, True, True, gbar=gb, peer_words=pw, peer_scales=ps)
+    dt = time.perf_counter() - t0
+    return {"value": 2 * n / dt, "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {nch} chunks ({n} params) of the same shard, W={W}: one "
+                      f"local+variance step and one sync+variance step, {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="gpt2-1.5b")
+    ap.add_argument("--cpu-sample-chunks", type=int, default=512)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the multi-GPU exchange of the method is not "
+              f"part of this build (asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2202_06009_amd as zo
+    import synth
+    from synth import configs as C
+
+    zo.lib()
+    wl = C.get(args.workload)
+    d, W = wl.n, wl.world
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    _, ln, word, nwords = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
+    nchunks = len(ln)
+    print(f"[bench] {wl.name}: d={d} W={W} chunk={wl.chunk} chunks={nchunks} words={nwords}",
+          file=sys.stderr, flush=True)
+
+    f32 = dict(dtype=torch.float32, device=dev)
+    state = {k: torch.empty(d, **f32) for k in ("x", "m", "v", "u", "err", "srv_err", "anchor")}
+    g = torch.empty(d, **f32)
+    gb = torch.empty(d, **f32)
+    packed = torch.empty((W, nwords), dtype=torch.int64, device=dev)
+    scales = torch.empty((W, nchunks), **f32)
+    srv_packed = torch.empty(nwords, dtype=torch.int64, device=dev)
+    srv_scales = torch.empty(nchunks, **f32)
+
+    ks = C.ksigma(wl.sigma_g)
+    synth.normal_dev(state["x"], 0, synth.key(0, C.STREAM_X, 0), C.ksigma(wl.sigma_x))
+    synth.normal_dev(g, 0, synth.key(0, C.STREAM_G, 0), ks, wl.outlier_per_mille,
+                     wl.outlier_factor)
+    synth.normal_dev(gb, 0, synth.key(0, C.STREAM_GBAR, 0), ks, wl.outlier_per_mille,
+                     wl.outlier_factor)
+    base = 2 * 1e-4 * 0.18 * wl.sigma_g
+    for w in range(1, W):
+        synth.bits_dev(packed[w], 0, synth.key(w, C.STREAM_BITS, 1))
+        synth.scales_dev(scales[w], 0, synth.key(w, C.STREAM_SCALES, 1), base)
+
+    total_steps = 2 * (args.warmup + args.steps)
+    opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=W, chunk=wl.chunk,
+                    seg_off=wl.seg_off, tv=list(range(total_steps)),
+                    tu=list(range(1, total_steps, 2)), state=state)
+    torch.cuda.synchronize()
+    gamma = 1e-4
+    names = ("local+var", "sync1", "srv", "recon+var")
+
+    def bench_step(k, ev=None):
+        t = 2 * k
+        calls = (
+            lambda: opt.local_step(t, gamma, g, gb),
+            lambda: opt.compress_pack_ef(t + 1, gamma, g, packed[0], scales[0]),
+            lambda: opt.unpack_average(t + 1, packed, scales, srv_packed, srv_scales),
+            lambda: opt.sync_update(t + 1, srv_packed, srv_scales, gb),
+        )
+        for i, call in enumerate(calls):
+            if ev is not None:
+                ev[i][0].record()
+            call()
+            if ev is not None:
+                ev[i][1].record()
+
+    for k in range(args.warmup):
+        bench_step(k)
+    torch.cuda.synchronize()
+    print("[bench] warmup done", file=sys.stderr, flush=True)
+
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in names]
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        bench_step(args.warmup + k, evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_kernel = {n: sum(evs[k][i][0].elapsed_time(evs[k][i][1]) for k in range(args.steps))
+                  / args.steps for i, n in enumerate(names)}
+    inexact = opt.inexact_chunks()
+    opt.close()
+
+    ms_per_step = wall * 1000.0 / args.steps
+    value = 2.0 * d / (ms_per_step / 1000.0)
+    bytes_ = algorithmic_bytes(d, nchunks, nwords, W)
+    kernels = {n: {"ms": round(per_kernel[n], 4),
+                   "gb_per_launch": round(bytes_[n] / 1e9, 3),
+                   "gbs": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0), 1),
+                   "frac": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0) / HBM_PEAK_GBS, 4)}
+               for n in names}
+    dom = max(names, key=lambda n: per_kernel[n])
+    step_bytes = sum(bytes_.values())
+    out = {
+        "metric": "0/1 Adam step params/sec and achieved HBM GB/s (% of peak), 1 MI355X",
+        "value": round(value, 1),
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name} flat shard, one local+variance step and one "
+                               f"sync+variance step per bench step",
+                   "params": d, "segments": wl.nseg, "world": W, "chunk": wl.chunk,
+                   "chunks": nchunks, "server": "single (all chunks)",
+                   "optimizer_steps_per_bench_step": 2},
+        "hbm_gbs_step": round(step_bytes / 1e9 / (ms_per_step / 1000.0), 1),
+        "hbm_frac_step": round(step_bytes / 1e9 / (ms_per_step / 1000.0) / HBM_PEAK_GBS, 4),
+        "kernels": kernels,
+        "inexact_chunks": inexact,
+        "roofline": {"bound": "hbm", "kernel": dom,
+                     "achieved": kernels[dom]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": kernels[dom]["frac"], "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_chunks)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

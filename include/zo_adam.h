@@ -1,0 +1,238 @@
+/*
+ * zo_adam.h -- C ABI of the MI355X (gfx950) hot path of 0/1 Adam.
+ *
+ * 0/1 Adam (Lu, Li, Zhang, De Sa, He, arXiv 2202.06009), Algorithm 1, with the
+ * error-feedback 1bit-AllReduce of Algorithm 2 and the 1-bit compressor of
+ * Equation 3, for ONE worker's flat binary32 parameter shard of length d.
+ * The other W-1 workers are represented only by their packed sign buffers and
+ * scales, which the caller places in device memory (slots 1..W-1 of a W-slot
+ * buffer); this worker writes its own into slot 0.
+ *
+ * Conventions shared by every entry point
+ *   - Device pointers are caller-owned HIP device allocations.  Float vectors
+ *     of shard length (state, g, gbar, avg_debug) must be 16-byte aligned,
+ *     packed word buffers 8-byte aligned, scale buffers 4-byte aligned
+ *     (ZO_EALIGN otherwise).  The library never frees or reallocates them.
+ *   - Every call validates all of its arguments on the host before enqueueing
+ *     anything; a rejected call returns a negative status and changes nothing.
+ *   - Calls are asynchronous on the stream given to zo_adam_init (or
+ *     zo_set_stream): they return after enqueueing one kernel.  Device faults
+ *     surface at the caller's synchronisation.
+ *   - No entry point after zo_adam_init allocates memory.
+ *   - A handle is not thread-safe; use one handle per stream.
+ *   - Arithmetic is IEEE binary32 with one rounding per operation, no FMA
+ *     contraction, correctly rounded division and square root, no flushing of
+ *     denormals; the per-chunk L1 norm is the balanced pairwise tree over the
+ *     chunk in index order; the server's average over workers is an exact sum
+ *     (binary64) divided by W and rounded once to binary32.
+ *
+ * Layout
+ *   - The shard is a list of segments (one per parameter tensor); every
+ *     segment is cut into chunks of at most `chunk` elements; Equation 3 is
+ *     applied to each chunk on its own.
+ *   - Packed signs: chunk c owns ceil(len_c / 64) uint64 words starting at
+ *     word_c = sum of the word counts of the chunks before it; element j of
+ *     the chunk is bit j % 64 of word j / 64 (LSB first); bit 1 means +1;
+ *     sign(0) = +1 for +0 and -0; pad bits are written as 0 and ignored on
+ *     input.  One binary32 scale per chunk.
+ *   - A W-slot packed buffer is uint64[W][wstride], scales float[W][cstride],
+ *     where wstride / cstride are the word / chunk counts of the server range
+ *     (all words / all chunks for the single server).
+ */
+#ifndef ZO_ADAM_H
+#define ZO_ADAM_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum {
+    ZO_OK = 0,
+    ZO_EINVAL = -1,   /* bad argument: null pointer, size, hyper-parameter, step */
+    ZO_EALIGN = -2,   /* pointer not 16-byte aligned / segment offset not a multiple of 4 */
+    ZO_ESTATE = -3,   /* call out of order for the current step */
+    ZO_EHIP = -4,     /* HIP runtime error (text via zo_last_hip_error) */
+    ZO_ENOMEM = -5    /* host or device allocation failed in zo_adam_init */
+};
+
+typedef struct zo_adam zo_adam;   /* opaque handle */
+
+/*
+ * Configuration (host memory, read during zo_adam_init only).
+ *   beta1, beta2   Adam decay factors, each in [0, 1) (Algorithm 1 inputs).
+ *   eps            numerical constant added inside the square root, >= 0.
+ *   world          number of workers n = W >= 1 (the average of Algorithm 2).
+ *   chunk          compression chunk length C: a multiple of 4 in [4, 16384].
+ *   n              shard length d >= 0.
+ *   nseg, seg_off  nseg >= 1 segments; seg_off[0] = 0, seg_off[nseg] = n,
+ *                  non-decreasing, every offset a multiple of 4.
+ *   ntv, tv        the variance-update step set T_v: strictly increasing
+ *                  0-based step indices (ntv may be 0).
+ *   ntu, tu        the synchronisation step set T_u, likewise.
+ *   srv_chunk_begin, srv_chunk_end
+ *                  chunk range [begin, end) that this GPU serves in the
+ *                  server half of Algorithm 2; end < 0 means "to the last
+ *                  chunk" (begin = 0, end = -1 is the single server).
+ */
+typedef struct zo_config {
+    float beta1, beta2, eps;
+    int32_t world;
+    int32_t chunk;
+    int64_t n;
+    int32_t nseg;
+    const int64_t *seg_off;
+    int32_t ntv;
+    const int64_t *tv;
+    int32_t ntu;
+    const int64_t *tu;
+    int64_t srv_chunk_begin, srv_chunk_end;
+} zo_config;
+
+/*
+ * Optimizer state (device memory, caller-owned, binary32).
+ *   x        model, float[n]; holds x_0 at init.
+ *   m, v, u  momentum, variance, local-step buffer, float[n].
+ *   err      worker compression error delta (Algorithm 2), float[n].
+ *   srv_err  server compression error (Algorithm 2), float[elements of the
+ *            server range].
+ *   anchor   model at the most recent synchronisation x_{t'}, float[n].
+ */
+typedef struct zo_state {
+    float *x, *m, *v, *u, *err, *srv_err, *anchor;
+} zo_state;
+
+/*
+ * zo_adam_init -- set up the handle (Algorithm 1, its "Require" line).
+ * Validates the configuration, builds the chunk table and copies it to the
+ * device (the only allocations the library makes), then enqueues on `stream`:
+ * m = v = u = err = srv_err = 0 and anchor = x.  Gamma = 0, next step t = 0.
+ * Returns ZO_OK and *h, or an error (then *h is NULL).
+ */
+int zo_adam_init(zo_adam **h, const zo_config *cfg, const zo_state *st, hipStream_t stream);
+
+/* Release the handle and its device chunk table.  Waits for the stream. */
+int zo_adam_destroy(zo_adam *h);
+
+/* Change the stream later calls enqueue on. */
+int zo_set_stream(zo_adam *h, hipStream_t stream);
+
+/*
+ * zo_local_step -- the momentum, model and buffer lines of Algorithm 1 for
+ * step t (must be the handle's next step), elementwise over the shard:
+ *   m' = beta1 m + (1 - beta1) g;  p = gamma m';
+ *   x <- x - p / sqrt(v + eps);  u <- u + p;  m <- m';  Gamma <- Gamma + gamma.
+ * The momentum used in the model and buffer lines is the fresh m' (the literal
+ * subscript t would freeze the momentum when every step synchronises).
+ *   gamma   learning rate gamma_t > 0, finite.
+ *   g       device float[n], this worker's stochastic gradient g_t.
+ *   gbar    NULL, or device float[n] with the full-precision average gradient
+ *           of step t when t is in T_v and t is not in T_u: the variance line
+ *           v <- beta2 v + (1 - beta2) gbar^2 is then fused (v_t is used above
+ *           before it is overwritten).  Passing gbar when t is not in T_v, or
+ *           when t is in T_u, is ZO_EINVAL.
+ * At t not in T_u this completes step t (unless the variance update is still
+ * due).  At t in T_u it is the unfused first half of a sync step:
+ * zo_compress_pack_ef with g = NULL must follow.
+ */
+int zo_local_step(zo_adam *h, int64_t t, float gamma, const float *g, const float *gbar);
+
+/*
+ * zo_compress_pack_ef -- worker half of Algorithm 2 applied to the buffer
+ * u_{t+1/2} at a sync step t in T_u (the 1bit-AllReduce line of Algorithm 1),
+ * with Equation 3 per chunk:
+ *   a = u_{t+1/2} + err;  s_c = |a|_1 / len_c (pairwise tree);
+ *   bit_j = (a_j >= 0);  err_j <- a_j - s_c (bit 1) or a_j + s_c (bit 0).
+ * With g != NULL the momentum/buffer lines are fused: u_{t+1/2} = u + gamma m'
+ * with m' = beta1 m + (1 - beta1) g, and Gamma += gamma; x, m and u are not
+ * written (the reconstruction supersedes them).  With g == NULL the call must
+ * follow zo_local_step(t) and u already holds u_{t+1/2} (gamma is ignored).
+ *   packed0  device uint64[words]: this worker's packed signs (slot 0).
+ *   scales0  device float[nchunks]: this worker's scales (slot 0).
+ */
+int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const float *g,
+                        uint64_t *packed0, float *scales0);
+
+/*
+ * zo_unpack_average -- server half of Algorithm 2 over the server chunk
+ * range, at sync step t, after zo_compress_pack_ef(t).  For each element:
+ *   avg = RN32( (sum_w (bit_w ? +S_w : -S_w)) / W )  (sum exact),
+ *   b = avg + srv_err;  per chunk s = |b|_1 / len_c;  sigma = (b >= 0);
+ *   srv_err <- b - s sigma.
+ * The line's "t+1" subscript on the averaged buffers is read as "t" (the
+ * error update on the same line uses t).
+ *   packed      device uint64[W][wstride]: slot w = worker w, slot 0 = own.
+ *   scales      device float[W][cstride], likewise.
+ *   srv_packed  device uint64[words] indexed by global word; only the server
+ *               range's words are written.
+ *   srv_scales  device float[nchunks] indexed by global chunk (range only).
+ *   avg_debug   NULL, or device float[range elements] receiving avg.
+ * The exact sum needs the nonzero scales of a chunk to span at most
+ * 29 - ceil(log2 W) binary exponents; chunks that violate it are counted
+ * (zo_inexact_chunks) and still produce the binary64 result.
+ */
+int zo_unpack_average(zo_adam *h, int64_t t, const uint64_t *packed, const float *scales,
+                      uint64_t *srv_packed, float *srv_scales, float *avg_debug);
+
+/*
+ * zo_sync_update -- the sync lines of Algorithm 1 at step t, after
+ * zo_unpack_average(t) (on a multi-GPU run, after the server outputs of all
+ * ranges have been gathered into srv_packed / srv_scales):
+ *   ubar = sigma s (the server's compressed average);
+ *   m <- ubar / Gamma;  x <- anchor - ubar / sqrt(v_t + eps);
+ *   anchor <- x;  u <- 0;  Gamma <- 0  (the next interval starts at t + 1).
+ *   srv_packed  device uint64[words], srv_scales device float[nchunks].
+ *   gbar        as in zo_local_step: fused variance line when t is in T_v.
+ */
+int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const float *srv_scales,
+                   const float *gbar);
+
+/*
+ * zo_variance_update -- the variance line of Algorithm 1 for t in T_v when it
+ * was not fused: v <- beta2 v + (1 - beta2) gbar^2, after the other calls of
+ * step t.  gbar: device float[n], the full-precision AllReduce output.
+ */
+int zo_variance_update(zo_adam *h, int64_t t, const float *gbar);
+
+/* ---- queries (host only; never touch the device unless stated) ---------- */
+int64_t zo_num_chunks(const zo_adam *h);
+int64_t zo_packed_words(const zo_adam *h);
+/* Server range: first chunk, chunk count, first word, word count, first
+ * element, element count (any pointer may be NULL). */
+int zo_server_range(const zo_adam *h, int64_t *chunk0, int64_t *nchunks, int64_t *word0,
+                    int64_t *nwords, int64_t *elem0, int64_t *nelems);
+/* Copy the chunk table to host arrays of nchunks entries (any may be NULL). */
+int zo_chunk_table(const zo_adam *h, int64_t *start, int64_t *len, int64_t *word);
+float zo_gamma_sum(const zo_adam *h);
+int64_t zo_next_step(const zo_adam *h);
+/* Number of server-range chunks whose scales broke the exact-sum condition
+ * in the most recent zo_unpack_average (synchronises the stream). */
+int zo_inexact_chunks(zo_adam *h, int64_t *count);
+const char *zo_strerror(int status);
+const char *zo_last_hip_error(const zo_adam *h);
+
+/* ---- diagnostics --------------------------------------------------------- */
+/* Elementwise q = a / b and r = sqrt(a) on the device, with the same binary32
+ * division and square root the kernels use (device float[n] each; async on
+ * `stream`).  Lets a test compare them with the host's IEEE operations. */
+int zo_diag_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,
+                    hipStream_t stream);
+
+/* ---- planning helpers (pure host; usable without a GPU) ----------------- */
+/* Validate a configuration exactly as zo_adam_init does. */
+int zo_config_check(const zo_config *cfg);
+/* Chunk count of a segment table, or a negative status. */
+int64_t zo_plan_num_chunks(int32_t nseg, const int64_t *seg_off, int32_t chunk);
+/* Fill a chunk table (arrays of zo_plan_num_chunks entries); returns the
+ * total packed word count or a negative status. */
+int64_t zo_plan_chunks(int32_t nseg, const int64_t *seg_off, int32_t chunk, int64_t *start,
+                       int64_t *len, int64_t *word);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ZO_ADAM_H */

@@ -1,0 +1,446 @@
+// zo_adam.cpp -- host side of the 0/1 Adam C ABI (include/zo_adam.h).
+//
+// Validates every call before launching anything, keeps the step state
+// machine of Algorithm 1 (which lines of step t have run), accumulates the
+// learning-rate sum Gamma of the current interval in binary32, and launches
+// exactly one kernel per call on the handle's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "zo_adam.h"
+#include "zo_internal.h"
+
+namespace {
+
+enum Phase {
+    PH_IDLE = 0,        // expecting the first call of step t
+    PH_LOCAL_SYNC = 1,  // zo_local_step ran at a sync step; compress (g = NULL) next
+    PH_COMPRESSED = 2,  // worker half of Algorithm 2 done
+    PH_AVERAGED = 3,    // server half done
+    PH_VAR_PENDING = 4  // only the variance line of step t is left
+};
+
+constexpr int32_t kMaxChunk = 16384;
+constexpr int32_t kMaxWorld = 1 << 16;
+
+inline bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+bool strictly_increasing(const int64_t *v, int32_t n)
+{
+    for (int32_t i = 0; i < n; ++i) {
+        if (v[i] < 0) return false;
+        if (i && v[i] <= v[i - 1]) return false;
+    }
+    return true;
+}
+
+int check_segments(int32_t nseg, const int64_t *seg_off, int32_t chunk)
+{
+    if (nseg < 1 || !seg_off) return ZO_EINVAL;
+    if (chunk < 4 || chunk > kMaxChunk || chunk % 4) return ZO_EINVAL;
+    if (seg_off[0] != 0) return ZO_EINVAL;
+    for (int32_t s = 0; s < nseg; ++s)
+        if (seg_off[s + 1] < seg_off[s]) return ZO_EINVAL;
+    for (int32_t s = 0; s <= nseg; ++s)
+        if (seg_off[s] % 4) return ZO_EALIGN;
+    return ZO_OK;
+}
+
+}  // namespace
+
+struct zo_adam {
+    zo::Scalars sc{};
+    int32_t world = 1, chunk = 4;
+    int64_t n = 0, nchunks = 0, nwords = 0;
+    std::vector<int64_t> hstart, hword;
+    std::vector<int32_t> hlen;
+    void *dtable = nullptr;
+    uint8_t *dflags = nullptr;
+    zo::Chunks ch{};
+    zo::Geometry geo{};
+    int64_t c0 = 0, c1 = 0, w0 = 0, w1 = 0, e0 = 0, e1 = 0;
+    zo_state st{};
+    hipStream_t stream = nullptr;
+    std::vector<int64_t> tv, tu;
+    int64_t t = 0;
+    int phase = PH_IDLE;
+    float gamma_sum = 0.0f;
+    int srv_algo = zo::SRV_AUTO;
+    char hip_err[192] = {0};
+
+    bool in_tv(int64_t s) const { return std::binary_search(tv.begin(), tv.end(), s); }
+    bool in_tu(int64_t s) const { return std::binary_search(tu.begin(), tu.end(), s); }
+
+    int hip_fail(hipError_t e)
+    {
+        std::snprintf(hip_err, sizeof hip_err, "%s: %s", hipGetErrorName(e), hipGetErrorString(e));
+        return ZO_EHIP;
+    }
+
+    // Step t is complete: advance.
+    void finish_step()
+    {
+        phase = PH_IDLE;
+        ++t;
+    }
+};
+
+extern "C" {
+
+int64_t zo_plan_num_chunks(int32_t nseg, const int64_t *seg_off, int32_t chunk)
+{
+    int rc = check_segments(nseg, seg_off, chunk);
+    if (rc) return rc;
+    int64_t total = 0;
+    for (int32_t s = 0; s < nseg; ++s) total += (seg_off[s + 1] - seg_off[s] + chunk - 1) / chunk;
+    return total;
+}
+
+int64_t zo_plan_chunks(int32_t nseg, const int64_t *seg_off, int32_t chunk, int64_t *start,
+                       int64_t *len, int64_t *word)
+{
+    int rc = check_segments(nseg, seg_off, chunk);
+    if (rc) return rc;
+    int64_t c = 0, w = 0;
+    for (int32_t s = 0; s < nseg; ++s) {
+        const int64_t end = seg_off[s + 1];
+        for (int64_t pos = seg_off[s]; pos < end; pos += chunk, ++c) {
+            const int64_t l = std::min<int64_t>(chunk, end - pos);
+            if (start) start[c] = pos;
+            if (len) len[c] = l;
+            if (word) word[c] = w;
+            w += (l + 63) / 64;
+        }
+    }
+    return w;
+}
+
+int zo_config_check(const zo_config *cfg)
+{
+    if (!cfg) return ZO_EINVAL;
+    const float b1 = cfg->beta1, b2 = cfg->beta2, e = cfg->eps;
+    if (!(b1 >= 0.0f && b1 < 1.0f) || !(b2 >= 0.0f && b2 < 1.0f)) return ZO_EINVAL;
+    if (!(e >= 0.0f) || !std::isfinite(e)) return ZO_EINVAL;
+    if (cfg->world < 1 || cfg->world > kMaxWorld) return ZO_EINVAL;
+    if (cfg->n < 0) return ZO_EINVAL;
+    int rc = check_segments(cfg->nseg, cfg->seg_off, cfg->chunk);
+    if (rc) return rc;
+    if (cfg->seg_off[cfg->nseg] != cfg->n) return ZO_EINVAL;
+    if (cfg->ntv < 0 || cfg->ntu < 0) return ZO_EINVAL;
+    if (cfg->ntv && (!cfg->tv || !strictly_increasing(cfg->tv, cfg->ntv))) return ZO_EINVAL;
+    if (cfg->ntu && (!cfg->tu || !strictly_increasing(cfg->tu, cfg->ntu))) return ZO_EINVAL;
+    const int64_t nch = zo_plan_num_chunks(cfg->nseg, cfg->seg_off, cfg->chunk);
+    const int64_t end = cfg->srv_chunk_end < 0 ? nch : cfg->srv_chunk_end;
+    if (cfg->srv_chunk_begin < 0 || cfg->srv_chunk_begin > end || end > nch) return ZO_EINVAL;
+    return ZO_OK;
+}
+
+int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStream_t stream)
+{
+    if (!out) return ZO_EINVAL;
+    *out = nullptr;
+    int rc = zo_config_check(cfg);
+    if (rc) return rc;
+    if (!st) return ZO_EINVAL;
+    const float *ptrs[] = {st->x, st->m, st->v, st->u, st->err, st->srv_err, st->anchor};
+    for (const float *p : ptrs) {
+        if (cfg->n > 0 && !p) return ZO_EINVAL;
+        if (!aligned(p, 16)) return ZO_EALIGN;
+    }
+
+    zo_adam *h = new (std::nothrow) zo_adam();
+    if (!h) return ZO_ENOMEM;
+    h->sc.b1 = cfg->beta1;
+    h->sc.b2 = cfg->beta2;
+    h->sc.eps = cfg->eps;
+    h->sc.c1 = 1.0f - cfg->beta1;
+    h->sc.c2 = 1.0f - cfg->beta2;
+    h->world = cfg->world;
+    h->chunk = cfg->chunk;
+    h->n = cfg->n;
+    h->geo = zo::geometry_for(cfg->chunk);
+    h->st = *st;
+    h->stream = stream;
+    h->tv.assign(cfg->tv, cfg->tv + cfg->ntv);
+    h->tu.assign(cfg->tu, cfg->tu + cfg->ntu);
+
+    h->nchunks = zo_plan_num_chunks(cfg->nseg, cfg->seg_off, cfg->chunk);
+    std::vector<int64_t> len64;
+    try {
+        h->hstart.resize(h->nchunks);
+        h->hword.resize(h->nchunks);
+        h->hlen.resize(h->nchunks);
+        len64.resize(h->nchunks);
+    } catch (...) {
+        delete h;
+        return ZO_ENOMEM;
+    }
+    h->nwords = zo_plan_chunks(cfg->nseg, cfg->seg_off, cfg->chunk, h->hstart.data(),
+                               len64.data(), h->hword.data());
+    for (int64_t c = 0; c < h->nchunks; ++c) h->hlen[c] = (int32_t)len64[c];
+
+    h->c0 = cfg->srv_chunk_begin;
+    h->c1 = cfg->srv_chunk_end < 0 ? h->nchunks : cfg->srv_chunk_end;
+    if (h->c1 > h->c0) {
+        h->e0 = h->hstart[h->c0];
+        h->e1 = h->hstart[h->c1 - 1] + h->hlen[h->c1 - 1];
+        h->w0 = h->hword[h->c0];
+        h->w1 = h->hword[h->c1 - 1] + (h->hlen[h->c1 - 1] + 63) / 64;
+    } else {
+        h->e0 = h->e1 = h->w0 = h->w1 = 0;
+    }
+
+    // Device chunk table + per-chunk exactness flags: the only allocations.
+    const size_t nb = (size_t)h->nchunks;
+    const size_t bytes = nb * (8 + 8 + 4) + (size_t)(h->c1 - h->c0) + 64;
+    if (nb) {
+        hipError_t e = hipMalloc(&h->dtable, bytes);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            delete h;
+            return e == hipErrorOutOfMemory ? ZO_ENOMEM : ZO_EHIP;
+        }
+        char *base = (char *)h->dtable;
+        h->ch.start = (const int64_t *)base;
+        h->ch.word = (const int64_t *)(base + nb * 8);
+        h->ch.len = (const int32_t *)(base + nb * 16);
+        h->dflags = (uint8_t *)(base + nb * 20);
+        hipError_t e1 = hipMemcpyAsync(base, h->hstart.data(), nb * 8, hipMemcpyHostToDevice,
+                                       stream);
+        hipError_t e2 = hipMemcpyAsync(base + nb * 8, h->hword.data(), nb * 8,
+                                       hipMemcpyHostToDevice, stream);
+        hipError_t e3 = hipMemcpyAsync(base + nb * 16, h->hlen.data(), nb * 4,
+                                       hipMemcpyHostToDevice, stream);
+        hipError_t e4 = hipMemsetAsync(h->dflags, 0, (size_t)(h->c1 - h->c0) + 1, stream);
+        if (e1 || e2 || e3 || e4) {
+            rc = h->hip_fail(e1 ? e1 : e2 ? e2 : e3 ? e3 : e4);
+            (void)hipStreamSynchronize(stream);
+            (void)hipFree(h->dtable);
+            delete h;
+            return rc;
+        }
+    }
+    // Require line of Algorithm 1: m = v = u = 0; errors start at 0
+    // (Algorithm 2); the anchor x_{t'} with t' = 0 is x_0.
+    if (h->n > 0) {
+        const size_t fb = (size_t)h->n * sizeof(float);
+        hipError_t es[6] = {
+            hipMemsetAsync(st->m, 0, fb, stream), hipMemsetAsync(st->v, 0, fb, stream),
+            hipMemsetAsync(st->u, 0, fb, stream), hipMemsetAsync(st->err, 0, fb, stream),
+            h->e1 > h->e0 ? hipMemsetAsync(st->srv_err, 0, (size_t)(h->e1 - h->e0) * 4, stream)
+                          : hipSuccess,
+            hipMemcpyAsync(st->anchor, st->x, fb, hipMemcpyDeviceToDevice, stream)};
+        for (hipError_t e : es) {
+            if (e != hipSuccess) {
+                rc = h->hip_fail(e);
+                (void)hipStreamSynchronize(stream);
+                if (h->dtable) (void)hipFree(h->dtable);
+                delete h;
+                return rc;
+            }
+        }
+    }
+    *out = h;
+    return ZO_OK;
+}
+
+int zo_adam_destroy(zo_adam *h)
+{
+    if (!h) return ZO_EINVAL;
+    int rc = ZO_OK;
+    hipError_t e = hipStreamSynchronize(h->stream);
+    if (e != hipSuccess) rc = h->hip_fail(e);
+    if (h->dtable) {
+        e = hipFree(h->dtable);
+        if (e != hipSuccess && rc == ZO_OK) rc = ZO_EHIP;
+    }
+    delete h;
+    return rc;
+}
+
+int zo_set_stream(zo_adam *h, hipStream_t stream)
+{
+    if (!h) return ZO_EINVAL;
+    h->stream = stream;
+    return ZO_OK;
+}
+
+static bool bad_gamma(float g) { return !(g > 0.0f) || !std::isfinite(g); }
+
+int zo_local_step(zo_adam *h, int64_t t, float gamma, const float *g, const float *gbar)
+{
+    if (!h) return ZO_EINVAL;
+    if (h->n > 0 && !g) return ZO_EINVAL;
+    if (bad_gamma(gamma)) return ZO_EINVAL;
+    if (!aligned(g, 16) || !aligned(gbar, 16)) return ZO_EALIGN;
+    if (h->phase != PH_IDLE || t != h->t) return ZO_ESTATE;
+    const bool tu = h->in_tu(t), tv = h->in_tv(t);
+    if (gbar && (!tv || tu)) return ZO_EINVAL;
+    zo::Scalars s = h->sc;
+    s.gamma = gamma;
+    hipError_t e = zo::launch_local(gbar != nullptr, g, h->st.m, h->st.x, h->st.v, h->st.u, gbar,
+                                    h->n, s, h->stream);
+    if (e != hipSuccess) return h->hip_fail(e);
+    h->gamma_sum = h->gamma_sum + gamma;
+    if (tu)
+        h->phase = PH_LOCAL_SYNC;
+    else if (tv && !gbar)
+        h->phase = PH_VAR_PENDING;
+    else
+        h->finish_step();
+    return ZO_OK;
+}
+
+int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const float *g, uint64_t *packed0,
+                        float *scales0)
+{
+    if (!h) return ZO_EINVAL;
+    if (h->nchunks > 0 && (!packed0 || !scales0)) return ZO_EINVAL;
+    if (!aligned(g, 16)) return ZO_EALIGN;
+    if (!aligned(packed0, 8) || !aligned(scales0, 4)) return ZO_EALIGN;
+    if (t != h->t || !h->in_tu(t)) return ZO_ESTATE;
+    const bool fused = g != nullptr;
+    if (fused) {
+        if (h->phase != PH_IDLE) return ZO_ESTATE;
+        if (bad_gamma(gamma)) return ZO_EINVAL;
+    } else if (h->phase != PH_LOCAL_SYNC) {
+        return ZO_ESTATE;
+    }
+    zo::Scalars s = h->sc;
+    s.gamma = fused ? gamma : 0.0f;
+    hipError_t e = zo::launch_sync1(h->geo, fused, g, h->st.m, h->st.u, h->st.err, h->ch,
+                                    h->nchunks, packed0, scales0, s, h->stream);
+    if (e != hipSuccess) return h->hip_fail(e);
+    if (fused) h->gamma_sum = h->gamma_sum + gamma;
+    h->phase = PH_COMPRESSED;
+    return ZO_OK;
+}
+
+int zo_unpack_average(zo_adam *h, int64_t t, const uint64_t *packed, const float *scales,
+                      uint64_t *srv_packed, float *srv_scales, float *avg_debug)
+{
+    if (!h) return ZO_EINVAL;
+    const int64_t nch = h->c1 - h->c0;
+    if (nch > 0 && (!packed || !scales || !srv_packed || !srv_scales)) return ZO_EINVAL;
+    if (!aligned(packed, 8) || !aligned(srv_packed, 8) || !aligned(scales, 4) ||
+        !aligned(srv_scales, 4) || !aligned(avg_debug, 16))
+        return ZO_EALIGN;
+    if (t != h->t || h->phase != PH_COMPRESSED) return ZO_ESTATE;
+    hipError_t e = zo::launch_srv(h->geo, h->srv_algo, packed, scales, h->world, h->w1 - h->w0,
+                                  nch, h->ch, h->c0, nch, h->w0, h->e0, h->st.srv_err,
+                                  srv_packed, srv_scales, avg_debug, h->dflags, h->stream);
+    if (e != hipSuccess) return h->hip_fail(e);
+    h->phase = PH_AVERAGED;
+    return ZO_OK;
+}
+
+int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const float *srv_scales,
+                   const float *gbar)
+{
+    if (!h) return ZO_EINVAL;
+    if (h->nchunks > 0 && (!srv_packed || !srv_scales)) return ZO_EINVAL;
+    if (!aligned(srv_packed, 8) || !aligned(srv_scales, 4) || !aligned(gbar, 16))
+        return ZO_EALIGN;
+    if (t != h->t || h->phase != PH_AVERAGED) return ZO_ESTATE;
+    const bool tv = h->in_tv(t);
+    if (gbar && !tv) return ZO_EINVAL;
+    hipError_t e = zo::launch_recon(h->geo, gbar != nullptr, srv_packed, srv_scales, h->ch,
+                                    h->nchunks, h->st.m, h->st.x, h->st.v, h->st.u, h->st.anchor,
+                                    gbar, h->gamma_sum, h->sc, h->stream);
+    if (e != hipSuccess) return h->hip_fail(e);
+    h->gamma_sum = 0.0f;
+    if (tv && !gbar)
+        h->phase = PH_VAR_PENDING;
+    else
+        h->finish_step();
+    return ZO_OK;
+}
+
+int zo_variance_update(zo_adam *h, int64_t t, const float *gbar)
+{
+    if (!h) return ZO_EINVAL;
+    if (h->n > 0 && !gbar) return ZO_EINVAL;
+    if (!aligned(gbar, 16)) return ZO_EALIGN;
+    if (t != h->t || h->phase != PH_VAR_PENDING) return ZO_ESTATE;
+    hipError_t e = zo::launch_var(h->st.v, gbar, h->n, h->sc, h->stream);
+    if (e != hipSuccess) return h->hip_fail(e);
+    h->finish_step();
+    return ZO_OK;
+}
+
+int64_t zo_num_chunks(const zo_adam *h) { return h ? h->nchunks : ZO_EINVAL; }
+int64_t zo_packed_words(const zo_adam *h) { return h ? h->nwords : ZO_EINVAL; }
+float zo_gamma_sum(const zo_adam *h) { return h ? h->gamma_sum : 0.0f; }
+int64_t zo_next_step(const zo_adam *h) { return h ? h->t : ZO_EINVAL; }
+
+int zo_server_range(const zo_adam *h, int64_t *chunk0, int64_t *nchunks, int64_t *word0,
+                    int64_t *nwords, int64_t *elem0, int64_t *nelems)
+{
+    if (!h) return ZO_EINVAL;
+    if (chunk0) *chunk0 = h->c0;
+    if (nchunks) *nchunks = h->c1 - h->c0;
+    if (word0) *word0 = h->w0;
+    if (nwords) *nwords = h->w1 - h->w0;
+    if (elem0) *elem0 = h->e0;
+    if (nelems) *nelems = h->e1 - h->e0;
+    return ZO_OK;
+}
+
+int zo_chunk_table(const zo_adam *h, int64_t *start, int64_t *len, int64_t *word)
+{
+    if (!h) return ZO_EINVAL;
+    for (int64_t c = 0; c < h->nchunks; ++c) {
+        if (start) start[c] = h->hstart[c];
+        if (len) len[c] = h->hlen[c];
+        if (word) word[c] = h->hword[c];
+    }
+    return ZO_OK;
+}
+
+int zo_inexact_chunks(zo_adam *h, int64_t *count)
+{
+    if (!h || !count) return ZO_EINVAL;
+    const int64_t nch = h->c1 - h->c0;
+    *count = 0;
+    if (nch <= 0) return ZO_OK;
+    std::vector<uint8_t> f((size_t)nch);
+    hipError_t e = hipMemcpyAsync(f.data(), h->dflags, (size_t)nch, hipMemcpyDeviceToHost,
+                                  h->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+    if (e != hipSuccess) return h->hip_fail(e);
+    int64_t c = 0;
+    for (uint8_t v : f) c += v ? 1 : 0;
+    *count = c;
+    return ZO_OK;
+}
+
+const char *zo_strerror(int status)
+{
+    switch (status) {
+    case ZO_OK: return "ok";
+    case ZO_EINVAL: return "invalid argument";
+    case ZO_EALIGN: return "misaligned pointer or segment offset";
+    case ZO_ESTATE: return "call out of order for the current step";
+    case ZO_EHIP: return "HIP runtime error";
+    case ZO_ENOMEM: return "out of memory";
+    default: return "unknown status";
+    }
+}
+
+const char *zo_last_hip_error(const zo_adam *h) { return h ? h->hip_err : ""; }
+
+int zo_diag_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,
+                    hipStream_t stream)
+{
+    if (n < 0 || (n > 0 && (!a || !b || !q || !r))) return ZO_EINVAL;
+    hipError_t e = zo::launch_divsqrt(a, b, q, r, n, stream);
+    return e == hipSuccess ? ZO_OK : ZO_EHIP;
+}
+
+}  // extern "C"

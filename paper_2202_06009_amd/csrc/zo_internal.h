@@ -1,0 +1,52 @@
+// zo_internal.h -- types shared by the host library and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace zo {
+
+// Binary32 scalars of one call; c1 = 1 - beta1 and c2 = 1 - beta2 are formed
+// in binary32 on the host once, so every kernel uses the same constants.
+struct Scalars {
+    float b1, c1, b2, c2, eps, gamma;
+};
+
+// Device chunk table: start element, length, first packed word.
+struct Chunks {
+    const int64_t *start;
+    const int32_t *len;
+    const int64_t *word;
+};
+
+// Mapping of one chunk onto a 256-thread workgroup: L lanes per chunk (a
+// power of two <= 256), V blocks of 4L elements per lane (a power of two,
+// > 1 only when L = 256).  4 * L * V >= the configured chunk length.
+struct Geometry {
+    int L, V;
+};
+
+Geometry geometry_for(int chunk);
+
+// Server-average algorithm.
+enum SrvAlgo { SRV_AUTO = 0, SRV_PLAIN = 1 };
+
+hipError_t launch_local(bool var, const float *g, float *m, float *x, float *v, float *u,
+                        const float *gbar, int64_t n, const Scalars &s, hipStream_t st);
+hipError_t launch_var(float *v, const float *gbar, int64_t n, const Scalars &s, hipStream_t st);
+hipError_t launch_sync1(Geometry geo, bool fused, const float *g, const float *m, const float *u,
+                        float *err, const Chunks &ch, int64_t nchunks, uint64_t *packed,
+                        float *scales, const Scalars &s, hipStream_t st);
+hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const float *scales, int W,
+                      int64_t wstride, int64_t cstride, const Chunks &ch, int64_t c0,
+                      int64_t nch, int64_t word0, int64_t elem0, float *srv_err,
+                      uint64_t *srv_packed, float *srv_scales, float *avg, uint8_t *flags,
+                      hipStream_t st);
+hipError_t launch_recon(Geometry geo, bool var, const uint64_t *srv_packed,
+                        const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
+                        float *x, float *v, float *u, float *anchor, const float *gbar,
+                        float gsum, const Scalars &s, hipStream_t st);
+hipError_t launch_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,
+                          hipStream_t st);
+
+}  // namespace zo

@@ -1,0 +1,104 @@
+"""CPU checks of the C-ABI library: it loads, exports every function the
+headers declare, and its host-only logic (validation, chunk planning) works
+without a GPU.  No kernel is launched here."""
+import glob
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2202_06009_amd as zo
+from synth import configs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        for m in re.finditer(r"^\s*[A-Za-z_][\w\s\*]*?\b(zo_\w+)\s*\(", text, flags=re.M):
+            names.add(m.group(1))
+    return names
+
+
+def test_library_exports_every_declared_function():
+    declared = header_functions()
+    assert {"zo_adam_init", "zo_local_step", "zo_compress_pack_ef", "zo_unpack_average",
+            "zo_sync_update", "zo_variance_update"} <= declared
+    out = subprocess.run(["nm", "-D", "--defined-only", zo.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    missing = declared - exported
+    assert not missing, missing
+    assert declared == set(zo.EXPORTS)
+    lib = zo.lib()
+    for name in declared:
+        assert hasattr(lib, name)
+
+
+def _cfg(**over):
+    d = dict(beta1=0.9, beta2=0.999, eps=1e-8, world=4, chunk=2048,
+             seg_off=[0, 4096, 8192], tv=[0, 1], tu=[1, 3])
+    d.update(over)
+    return d
+
+
+@pytest.mark.parametrize("over,code", [
+    ({}, zo.ZO_OK),
+    ({"beta1": 1.0}, zo.ZO_EINVAL),
+    ({"beta1": -0.1}, zo.ZO_EINVAL),
+    ({"beta2": float("nan")}, zo.ZO_EINVAL),
+    ({"eps": -1e-8}, zo.ZO_EINVAL),
+    ({"eps": float("inf")}, zo.ZO_EINVAL),
+    ({"world": 0}, zo.ZO_EINVAL),
+    ({"chunk": 0}, zo.ZO_EINVAL),
+    ({"chunk": 6}, zo.ZO_EINVAL),
+    ({"chunk": 16388}, zo.ZO_EINVAL),
+    ({"chunk": 16384}, zo.ZO_OK),
+    ({"chunk": 4}, zo.ZO_OK),
+    ({"seg_off": [0, 4098, 8192]}, zo.ZO_EALIGN),
+    ({"seg_off": [4, 8192]}, zo.ZO_EINVAL),
+    ({"seg_off": [0, 8192, 4096]}, zo.ZO_EINVAL),
+    ({"seg_off": [0, 0, 0]}, zo.ZO_OK),
+    ({"tv": [1, 1]}, zo.ZO_EINVAL),
+    ({"tu": [3, 1]}, zo.ZO_EINVAL),
+    ({"tu": [-1]}, zo.ZO_EINVAL),
+    ({"srv_chunk_begin": 1, "srv_chunk_end": 3}, zo.ZO_OK),
+    ({"srv_chunk_begin": 3, "srv_chunk_end": 5}, zo.ZO_EINVAL),
+    ({"srv_chunk_begin": 2, "srv_chunk_end": 1}, zo.ZO_EINVAL),
+])
+def test_config_validation(over, code):
+    assert zo.zo_config_check(**_cfg(**over)) == code
+
+
+@pytest.mark.parametrize("name", ["tiny", "bert-base", "resnet50", "gpt2-1.5b"])
+def test_chunk_plan_matches_oracle_layout(name):
+    """Two independent chunkings of the same segment table agree."""
+    import oracle as orc
+    wl = configs.get(name)
+    start, ln, word, nw = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
+    lay = orc.Layout.from_segments(wl.seg_off, wl.chunk)
+    np.testing.assert_array_equal(start, lay.cstart)
+    np.testing.assert_array_equal(ln, lay.clen)
+    np.testing.assert_array_equal(word, lay.cword)
+    assert nw == lay.nwords
+
+
+def test_chunk_plan_counts_match_survey_shapes():
+    expect = {"tiny": (512, 0), "bert-base": (26823, 125), "bert-large": (41116, 245),
+              "resnet50": (25021, 86), "gpt2-1.5b": (95442, 483)}
+    for name, (nch, partial) in expect.items():
+        wl = configs.get(name)
+        _, ln, _, _ = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
+        assert len(ln) == nch
+        assert sum(1 for l in ln if l != wl.chunk) == partial
+
+
+def test_unbuilt_library_raises(monkeypatch, tmp_path):
+    monkeypatch.setattr(zo, "_lib", None)
+    monkeypatch.setattr(zo, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        zo.lib()

@@ -1,0 +1,167 @@
+"""GPU parity: the HIP library against the CPU oracle, bit for bit.
+
+Every state (x, m, v, u, worker error, server error, anchor), the own packed
+signs and scales and the server packed signs and scales are compared after
+every step of a run.  The contract allows a relative error of 1e-6 on the
+binary32 states; the kernels are built to reproduce the oracle's rounding
+exactly, so these tests demand equality (with -0 == +0), which implies it.
+"""
+import numpy as np
+import pytest
+
+from synth import configs as C
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+@pytest.fixture(autouse=True)
+def _free_memory(torch_cuda):
+    yield
+    import gc
+    gc.collect()
+    torch_cuda.cuda.empty_cache()
+
+
+def _log(msg):
+    print(msg, flush=True)
+
+
+def _assert_clean(report, inexact):
+    for t, bad in enumerate(report):
+        assert not bad, f"mismatch after step {t - 1}: {bad}"
+    assert inexact == 0
+
+
+# ---------------------------------------------------------------------------
+# the binary32 division and square root the kernels use
+# ---------------------------------------------------------------------------
+
+def test_device_div_sqrt_are_correctly_rounded(torch_cuda):
+    import paper_2202_06009_amd as zo
+    torch = torch_cuda
+    r = np.random.default_rng(0)
+    n = 1 << 24
+    # random finite bit patterns (both signs, all exponents incl. denormals)
+    a = r.integers(0, 0x7F800000, size=n, dtype=np.uint32).view(np.float32).copy()
+    b = r.integers(0, 0x7F800000, size=n, dtype=np.uint32).view(np.float32).copy()
+    b[r.random(n) < 0.5] *= -1
+    # values like the optimizer's: v + eps around 1e-8 .. 1e-2, ubar ~ 1e-8
+    a[: n // 4] = (r.random(n // 4) * 1e-2 + 1e-8).astype(np.float32)
+    b[: n // 4] = (r.standard_normal(n // 4) * 1e-4).astype(np.float32)
+    ta, tb = torch.from_numpy(a).cuda(), torch.from_numpy(b).cuda()
+    tq, tr = torch.empty_like(ta), torch.empty_like(ta)
+    zo.zo_diag_divsqrt(ta, tb, tq, tr)
+    torch.cuda.synchronize()
+    with np.errstate(all="ignore"):
+        q_ref = a / b
+        r_ref = np.sqrt(a)
+    q, rr = tq.cpu().numpy(), tr.cpu().numpy()
+    assert np.array_equal(q.view(np.uint32), q_ref.view(np.uint32))
+    assert np.array_equal(rr.view(np.uint32), r_ref.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# Tiny workload, whole shard, both readings of its schedule
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["tiny", "tiny-alt"])
+@pytest.mark.parametrize("fused", [True, False])
+def test_tiny_full_shard(torch_cuda, name, fused):
+    import harness
+    report, inexact = harness.run_parity(C.get(name), fused=fused, log=_log)
+    _assert_clean(report, inexact)
+    assert len(report) == C.get(name).steps + 1
+
+
+# ---------------------------------------------------------------------------
+# small ragged layouts: every kernel geometry, ragged tails, empty segments
+# ---------------------------------------------------------------------------
+
+def _small(name, segs, chunk, world, steps=8, tu=None, tv=None, sigma=1e-3, gammas=None):
+    T = steps
+    return C.Workload(
+        name=name, seg_off=C.offsets(segs), world=world, chunk=chunk, steps=T,
+        tv=tv if tv is not None else [0, 1, 2, 5],
+        tu=tu if tu is not None else [t for t in range(T) if t % 3 != 0],
+        gammas=gammas or [1e-4 * (1 + 0.25 * t) for t in range(T)], sigma_g=sigma)
+
+
+SMALL = [
+    # (segments, chunk, W): chunk sets the lanes-per-chunk L and blocks V
+    ([100, 4, 36, 0, 260], 4, 3),            # L = 1
+    ([96, 12, 8, 40], 8, 2),                 # L = 2
+    ([132, 16, 0, 64], 16, 5),               # L = 4
+    ([200, 32, 4], 28, 1),                   # L = 8, chunk not a power of two
+    ([1000, 64, 60], 64, 4),                 # L = 16
+    ([1000, 128, 124, 4], 100, 8),           # L = 32
+    ([3000, 256, 252], 256, 16),             # L = 64
+    ([5000, 512, 4, 508], 500, 3),           # L = 128
+    ([9000, 1024, 1020, 8], 1024, 4),        # L = 256
+    ([20000, 2048, 4], 2048, 2),             # V = 2
+    ([12000, 2500, 4000], 3000, 7),          # V = 4 with a non-power-of-two chunk
+    ([40000, 8192, 8188], 8192, 4),          # V = 8
+    ([70000, 16384, 16380, 4], 16384, 3),    # V = 16
+]
+
+
+@pytest.mark.parametrize("segs,chunk,world", SMALL, ids=[f"C{c}-W{w}" for _, c, w in SMALL])
+def test_small_layouts_full_shard(torch_cuda, segs, chunk, world):
+    import harness
+    wl = _small(f"small-C{chunk}", segs, chunk, world)
+    report, inexact = harness.run_parity(wl, log=_log)
+    _assert_clean(report, inexact)
+
+
+def test_single_worker_every_step_syncs(torch_cuda):
+    """W = 1 with a sync and a variance update at every step (the setting in
+    which the method reduces to Adam) -- exercises the fused variance line in
+    the reconstruction at every step."""
+    import harness
+    T = 10
+    wl = _small("w1-adam", [8192, 4096, 1000], 1024, 1, steps=T, tu=list(range(T)),
+                tv=list(range(T)))
+    report, inexact = harness.run_parity(wl, log=_log)
+    _assert_clean(report, inexact)
+
+
+def test_local_steps_only(torch_cuda):
+    import harness
+    T = 12
+    wl = _small("local-only", [50000, 4096], 2048, 4, steps=T, tu=[], tv=[0, 3, 7])
+    report, inexact = harness.run_parity(wl, log=_log)
+    _assert_clean(report, inexact)
+
+
+# ---------------------------------------------------------------------------
+# the paper-shaped workloads at full size, chunk-sampled oracle
+# ---------------------------------------------------------------------------
+
+SAMPLED = {
+    "resnet50": (300000, 1500),
+    "bert-base": (600000, 3000),
+    "bert-large": (600000, 5000),
+    "gpt2-1.5b": (500000, 12000),
+}
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", list(SAMPLED))
+def test_workload_sampled(torch_cuda, name):
+    import harness
+    import oracle as orc
+    wl = C.get(name)
+    lay = orc.Layout.from_segments(wl.seg_off, wl.chunk)
+    budget, stride = SAMPLED[name]
+    ids = harness.sample_chunks(lay, wl.seg_off, budget, stride)
+    _log(f"{name}: {len(ids)} chunks sampled, {int(lay.clen[ids].sum())} elements, "
+         f"{int((lay.clen[ids] != wl.chunk).sum())} ragged")
+    report, inexact = harness.run_parity(wl, chunk_ids=ids, log=_log)
+    _assert_clean(report, inexact)
