@@ -334,7 +334,8 @@ int zo_unpack_average(zo_adam *h, int64_t t, const uint64_t *packed, const float
     if (t != h->t || h->phase != PH_COMPRESSED) return ZO_ESTATE;
     hipError_t e = zo::launch_srv(h->geo, h->srv_algo, packed, scales, h->world, h->w1 - h->w0,
                                   nch, h->ch, h->c0, nch, h->w0, h->e0, h->st.srv_err,
-                                  srv_packed, srv_scales, avg_debug, h->dflags, h->stream);
+                                  srv_packed, srv_scales, avg_debug, h->dflags, h->chunk,
+                                  h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     h->phase = PH_AVERAGED;
     return ZO_OK;

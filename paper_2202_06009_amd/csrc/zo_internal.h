@@ -41,7 +41,7 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
                       int64_t wstride, int64_t cstride, const Chunks &ch, int64_t c0,
                       int64_t nch, int64_t word0, int64_t elem0, float *srv_err,
                       uint64_t *srv_packed, float *srv_scales, float *avg, uint8_t *flags,
-                      hipStream_t st);
+                      int chunk, hipStream_t st);
 hipError_t launch_recon(Geometry geo, bool var, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const float *gbar,

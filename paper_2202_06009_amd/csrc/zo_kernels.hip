@@ -376,6 +376,190 @@ __global__ __launch_bounds__(256) void k_srv_plain(const uint32_t *__restrict__ 
     if (active && lc == 0) flags[cr] = (uint8_t)f;
 }
 
+// Server with a lookup table per group of 8 workers ("four Russians"): for a
+// chunk, T_g[b] = sum_{k<8} (bit k of b ? +S_{8g+k} : -S_{8g+k}) in binary64
+// for all 256 bytes b; an element's sum over W workers is then the sum over
+// groups of T_g[byte of its 8 workers' bits].  Under the exact-sum condition
+// every partial sum is exact, so any grouping gives the bits of the
+// sequential sum.  Lane mapping: one lane owns the 32 elements of one packed
+// dword per round (round r, lane lc -> dword r*LD + lc of the chunk); the
+// 8 x 32 bit block of a worker group is transposed in registers so that byte c
+// of register k holds element 8c+k's 8 worker bits.
+__device__ __forceinline__ void transpose8x32(uint32_t (&x)[8])
+{
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        uint32_t t = ((x[k] >> 4) ^ x[k + 4]) & 0x0F0F0F0Fu;
+        x[k + 4] ^= t;
+        x[k] ^= t << 4;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; k += (k & 1) ? 3 : 1) {   // pairs (0,2) (1,3) (4,6) (5,7)
+        uint32_t t = ((x[k] >> 2) ^ x[k + 2]) & 0x33333333u;
+        x[k + 2] ^= t;
+        x[k] ^= t << 2;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; k += 2) {
+        uint32_t t = ((x[k] >> 1) ^ x[k + 1]) & 0x55555555u;
+        x[k + 1] ^= t;
+        x[k] ^= t << 1;
+    }
+}
+
+// In-lane pairwise tree of |v[0..32)| in index order.
+__device__ __forceinline__ float tree32_abs(const float (&v)[32])
+{
+    float t[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) t[i] = fabsf(v[i]);
+#pragma unroll
+    for (int w = 1; w < 32; w <<= 1) {
+#pragma unroll
+        for (int i = 0; i + w < 32; i += 2 * w) t[i] = t[i] + t[i + w];
+    }
+    return t[0];
+}
+
+template <int LD, int R>
+__global__ __launch_bounds__(256) void k_srv_lut(const uint32_t *__restrict__ packed32,
+                                                 const float *__restrict__ scales, int W, int G,
+                                                 int64_t wstride, int64_t cstride, Chunks ch,
+                                                 int64_t c0, int64_t nch, int64_t word0,
+                                                 int64_t elem0, float *__restrict__ srv_err,
+                                                 uint32_t *__restrict__ srv_packed32,
+                                                 float *__restrict__ srv_scales,
+                                                 float *__restrict__ avg_out,
+                                                 uint8_t *__restrict__ flags, int cpw,
+                                                 double inv_w, int w_pow2)
+{
+    extern __shared__ double dyn_lds[];
+    double *tab = dyn_lds;                                   // [cpw][G][256]
+    float *sc = reinterpret_cast<float *>(tab + (size_t)cpw * G * 256);  // [cpw][W]
+    float *tree = sc + (((size_t)cpw * W + 3) & ~(size_t)3); // [64]
+
+    const int q = threadIdx.x / LD, lc = threadIdx.x % LD;
+    const int64_t cbase = (int64_t)blockIdx.x * cpw;
+    const int64_t cr = cbase + q;
+    const bool active = cr < nch;
+    const int64_t c = c0 + (active ? cr : 0);
+    const int len = active ? ch.len[c] : 0;
+    const int64_t el = active ? ch.start[c] - elem0 : 0;
+    const int64_t wd = active ? ch.word[c] - word0 : 0;
+
+    // stage the scales of the workgroup's chunks, then build the tables
+    for (int i = threadIdx.x; i < cpw * W; i += blockDim.x) {
+        const int qq = i / W, w = i - qq * W;
+        sc[i] = (cbase + qq < nch) ? scales[cstride * w + cbase + qq] : 0.0f;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < cpw * G * 256; i += blockDim.x) {
+        const int qq = i / (G * 256), g = (i >> 8) % G, b = i & 255;
+        double t = 0.0;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int w = 8 * g + k;
+            if (w < W) {
+                const double sw = (double)sc[qq * W + w];
+                t += ((b >> k) & 1) ? sw : -sw;
+            }
+        }
+        tab[i] = t;
+    }
+    __syncthreads();
+    const double *mytab = tab + (size_t)q * G * 256;
+
+    const int ndw_data = (len + 31) >> 5;
+    float bv[R][32];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int j = r * LD + lc;
+        double acc[32];
+#pragma unroll
+        for (int i = 0; i < 32; ++i) acc[i] = 0.0;
+        if (j < ndw_data) {
+            const uint32_t *src = packed32 + 2 * wd + j;
+            const int64_t ws = 2 * wstride;
+            for (int g = 0; g < G; ++g) {
+                uint32_t x[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const int w = 8 * g + k;
+                    x[k] = (w < W) ? src[ws * w] : 0u;
+                }
+                transpose8x32(x);
+                const double *tg = mytab + g * 256;
+#pragma unroll
+                for (int cc = 0; cc < 4; ++cc) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) acc[8 * cc + k] += tg[(x[k] >> (8 * cc)) & 0xFFu];
+                }
+            }
+        }
+#pragma unroll
+        for (int i4 = 0; i4 < 8; ++i4) {
+            const int e = 32 * j + 4 * i4;
+            if (e < len) {
+                float4 av;
+                if (w_pow2) {
+                    av.x = (float)(acc[4 * i4 + 0] * inv_w);
+                    av.y = (float)(acc[4 * i4 + 1] * inv_w);
+                    av.z = (float)(acc[4 * i4 + 2] * inv_w);
+                    av.w = (float)(acc[4 * i4 + 3] * inv_w);
+                } else {
+                    av.x = (float)(acc[4 * i4 + 0] / (double)W);
+                    av.y = (float)(acc[4 * i4 + 1] / (double)W);
+                    av.z = (float)(acc[4 * i4 + 2] / (double)W);
+                    av.w = (float)(acc[4 * i4 + 3] / (double)W);
+                }
+                if (avg_out) st4(avg_out, (el + e) >> 2, av);
+                const float4 d = ld4(srv_err, (el + e) >> 2);
+                bv[r][4 * i4 + 0] = av.x + d.x;
+                bv[r][4 * i4 + 1] = av.y + d.y;
+                bv[r][4 * i4 + 2] = av.z + d.z;
+                bv[r][4 * i4 + 3] = av.w + d.w;
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) bv[r][4 * i4 + i] = 0.0f;
+            }
+        }
+    }
+
+    // Equation 3 with the server error, in the same lane layout
+    float part[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) part[r] = tree32_abs(bv[r]);
+    const float tot = chunk_tree<LD, R>(part, tree);
+    const float s = tot / (float)len;
+    const int ndw = 2 * ((len + 63) >> 6);
+    uint32_t *dst = srv_packed32 + 2 * (active ? ch.word[c] : 0);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int j = r * LD + lc;
+        uint32_t bits = 0;
+#pragma unroll
+        for (int i4 = 0; i4 < 8; ++i4) {
+            const int e = 32 * j + 4 * i4;
+            if (active && e < len) {
+                float4 bb = make_float4(bv[r][4 * i4], bv[r][4 * i4 + 1], bv[r][4 * i4 + 2],
+                                        bv[r][4 * i4 + 3]);
+                float4 d;
+                d.x = ef_elem(bb.x, s);
+                d.y = ef_elem(bb.y, s);
+                d.z = ef_elem(bb.z, s);
+                d.w = ef_elem(bb.w, s);
+                st4(srv_err, (el + e) >> 2, d);
+                bits |= sign4(bb) << (4 * i4);
+            }
+        }
+        if (active && j < ndw) dst[j] = bits;
+    }
+    if (LD * R == 1 && active && ndw > 1) dst[1] = 0u;
+    if (active && lc == 0) srv_scales[c] = s;
+    const uint32_t f = inexact_flag<LD>(scales + (active ? cr : 0), cstride, W, lc);
+    if (active && lc == 0) flags[cr] = (uint8_t)f;
+}
+
 // ---------------------------------------------------------------------------
 // a5 (+a2): reconstruct momentum and model from the server's compressed
 // average; reset the buffer; move the anchor
@@ -552,23 +736,69 @@ hipError_t launch_sync1(Geometry geo, bool fused, const float *g, const float *m
     });
 }
 
+// Lanes per chunk and rounds of the LUT server: one lane per packed dword.
+static inline Geometry srv_geometry_for(int chunk)
+{
+    const int dws = (chunk + 31) / 32;
+    if (dws <= 256) return Geometry{next_pow2(dws), 1};
+    return Geometry{256, next_pow2((dws + 255) / 256)};
+}
+
+static constexpr size_t kSrvLdsMax = 64 * 1024;
+
 hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const float *scales, int W,
                       int64_t wstride, int64_t cstride, const Chunks &ch, int64_t c0,
                       int64_t nch, int64_t word0, int64_t elem0, float *srv_err,
                       uint64_t *srv_packed, float *srv_scales, float *avg, uint8_t *flags,
-                      hipStream_t st)
+                      int chunk, hipStream_t st)
 {
-    (void)algo;
     if (nch == 0) return hipSuccess;
-    return with_geometry(geo, [&](auto Lc, auto Vc) {
-        constexpr int L = decltype(Lc)::value, V = decltype(Vc)::value;
-        const unsigned grid = (unsigned)((nch + (256 / L) - 1) / (256 / L));
-        hipLaunchKernelGGL((k_srv_plain<L, V>), dim3(grid), dim3(256), 0, st,
-                           reinterpret_cast<const uint32_t *>(packed), scales, W, wstride,
+    const int G = (W + 7) / 8;
+    const size_t per_chunk = (size_t)G * 256 * 8 + (size_t)W * 4 + 16;
+    const Geometry sg = srv_geometry_for(chunk);
+    const bool lut = algo != SRV_PLAIN && sg.V <= 2 && per_chunk + 256 <= kSrvLdsMax;
+    if (!lut) {
+        return with_geometry(geo, [&](auto Lc, auto Vc) {
+            constexpr int L = decltype(Lc)::value, V = decltype(Vc)::value;
+            const unsigned grid = (unsigned)((nch + (256 / L) - 1) / (256 / L));
+            hipLaunchKernelGGL((k_srv_plain<L, V>), dim3(grid), dim3(256), 0, st,
+                               reinterpret_cast<const uint32_t *>(packed), scales, W, wstride,
+                               cstride, ch, c0, nch, word0, elem0, srv_err,
+                               reinterpret_cast<uint32_t *>(srv_packed), srv_scales, avg, flags);
+            return hipGetLastError();
+        });
+    }
+    int cpw = 256 / sg.L;
+    while (cpw > 1 && (size_t)cpw * per_chunk + 256 > kSrvLdsMax) cpw >>= 1;
+    const size_t lds = (size_t)cpw * ((size_t)G * 256 * 8) + (((size_t)cpw * W + 3) & ~(size_t)3) * 4 +
+                       64 * 4;
+    const bool pow2 = (W & (W - 1)) == 0;
+    const double inv_w = 1.0 / (double)W;
+    const unsigned grid = (unsigned)((nch + cpw - 1) / cpw);
+    const unsigned block = (unsigned)(sg.L * cpw);
+    auto go = [&](auto Lc, auto Rc) {
+        constexpr int L = decltype(Lc)::value, Rr = decltype(Rc)::value;
+        hipLaunchKernelGGL((k_srv_lut<L, Rr>), dim3(grid), dim3(block), lds, st,
+                           reinterpret_cast<const uint32_t *>(packed), scales, W, G, wstride,
                            cstride, ch, c0, nch, word0, elem0, srv_err,
-                           reinterpret_cast<uint32_t *>(srv_packed), srv_scales, avg, flags);
+                           reinterpret_cast<uint32_t *>(srv_packed), srv_scales, avg, flags, cpw,
+                           inv_w, pow2 ? 1 : 0);
         return hipGetLastError();
-    });
+    };
+    using std::integral_constant;
+    if (sg.V == 2) return go(integral_constant<int, 256>{}, integral_constant<int, 2>{});
+    switch (sg.L) {
+    case 1: return go(integral_constant<int, 1>{}, integral_constant<int, 1>{});
+    case 2: return go(integral_constant<int, 2>{}, integral_constant<int, 1>{});
+    case 4: return go(integral_constant<int, 4>{}, integral_constant<int, 1>{});
+    case 8: return go(integral_constant<int, 8>{}, integral_constant<int, 1>{});
+    case 16: return go(integral_constant<int, 16>{}, integral_constant<int, 1>{});
+    case 32: return go(integral_constant<int, 32>{}, integral_constant<int, 1>{});
+    case 64: return go(integral_constant<int, 64>{}, integral_constant<int, 1>{});
+    case 128: return go(integral_constant<int, 128>{}, integral_constant<int, 1>{});
+    case 256: return go(integral_constant<int, 256>{}, integral_constant<int, 1>{});
+    default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_recon(Geometry geo, bool var, const uint64_t *srv_packed,

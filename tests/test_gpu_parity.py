@@ -109,6 +109,8 @@ SMALL = [
     ([12000, 2500, 4000], 3000, 7),          # V = 4 with a non-power-of-two chunk
     ([40000, 8192, 8188], 8192, 4),          # V = 8
     ([70000, 16384, 16380, 4], 16384, 3),    # V = 16
+    ([5000, 1000, 96], 1024, 9),             # two worker groups, the second partial
+    ([5000, 1000], 1024, 300),               # tables beyond the LDS budget: plain server
 ]
 
 
