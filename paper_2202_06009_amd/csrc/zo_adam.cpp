@@ -353,7 +353,7 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
     if (gbar && !tv) return ZO_EINVAL;
     hipError_t e = zo::launch_recon(h->geo, gbar != nullptr, srv_packed, srv_scales, h->ch,
                                     h->nchunks, h->st.m, h->st.x, h->st.v, h->st.u, h->st.anchor,
-                                    gbar, h->gamma_sum, h->sc, h->stream);
+                                    gbar, h->gamma_sum, h->sc, h->chunk, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     h->gamma_sum = 0.0f;
     if (tv && !gbar)

@@ -19,9 +19,10 @@ struct Chunks {
     const int64_t *word;
 };
 
-// Mapping of one chunk onto a 256-thread workgroup: L lanes per chunk (a
-// power of two <= 256), V blocks of 4L elements per lane (a power of two,
-// > 1 only when L = 256).  4 * L * V >= the configured chunk length.
+// Mapping of one chunk onto a workgroup: L lanes per chunk (a power of two
+// <= 1024; several chunks share a 256-thread workgroup when L < 256), V blocks
+// of 4L elements per lane (a power of two, > 1 only when L = 1024).
+// 4 * L * V >= the configured chunk length.
 struct Geometry {
     int L, V;
 };
@@ -45,7 +46,7 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
 hipError_t launch_recon(Geometry geo, bool var, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const float *gbar,
-                        float gsum, const Scalars &s, hipStream_t st);
+                        float gsum, const Scalars &s, int chunk, hipStream_t st);
 hipError_t launch_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,
                           hipStream_t st);
 

@@ -4,47 +4,60 @@
 // Training via 0/1 Adam" (arXiv 2202.06009): Algorithm 1 (0/1 Adam),
 // Algorithm 2 (error-feedback 1bit-AllReduce), Equation 3 (1-bit compressor).
 //
-// Every kernel is HBM-streaming: no contraction, so no MFMA.  Arithmetic is
-// binary32 with one rounding per operation (the library is built with
-// -ffp-contract=off; division and sqrtf are the correctly rounded lowerings),
-// so results are reproducible bit for bit by any implementation that follows
-// the same operation order.
+// Every kernel streams HBM: nothing is a contraction, so nothing uses MFMA.
+// Arithmetic is binary32 with one rounding per operation (the library is
+// built with -ffp-contract=off; division and sqrtf are the correctly rounded
+// lowerings), so any implementation that follows the same operation order
+// reproduces the results bit for bit.
 //
-// Data layout
-//   * state vectors are flat float[n], n a multiple of 4, accessed as float4;
-//   * chunk kernels map one chunk onto L lanes (L a power of two <= 256) of a
-//     256-thread workgroup; lane lc of the chunk holds, for each block k < V,
-//     the four elements 4*L*k + 4*lc + {0,1,2,3}.  A block of 4L elements is
-//     therefore one contiguous, coalesced 16*L-byte span per buffer;
-//   * per-chunk L1 norm: in-lane (|a0|+|a1|)+(|a2|+|a3|), then an xor
-//     butterfly over the lanes of a wave (pairs partner lanes l and l^o, i.e.
-//     adjacent index ranges), then an in-order tree over the chunk's waves and
-//     over its blocks.  That is exactly the balanced pairwise tree over the
-//     chunk in index order; the zero padding beyond the chunk length adds +0
-//     and changes no bit;
-//   * packed signs: dword j of a chunk's words holds elements 32j..32j+31,
-//     assembled by an OR butterfly over 8 lanes (4 bits per lane) and stored
-//     by every 8th lane.
+// Memory access
+//   * every state vector is read and written once per step with 16-byte
+//     nontemporal loads and stores where a wave's access covers whole cache
+//     lines (each byte is touched once: keeping it out of the caches leaves
+//     them to the small shared data); lane-strided accesses, where a lane
+//     walks its own line in several loads, stay plain so that the line is
+//     fetched once;
+//   * elementwise kernels give one float4 to each thread of a grid that covers
+//     the whole shard, so the workgroups in flight cover a compact, contiguous
+//     address window; the reconstruction uses the same shape within chunks
+//     (one 256-thread workgroup per 1024-element block of a chunk);
+//   * chunk kernels (compress, server) need a chunk's L1 norm before any of its
+//     outputs can be written, so one workgroup owns a whole chunk and keeps it
+//     in registers: one pass over HBM.
+//
+// Chunk layout in a workgroup: L lanes per chunk (a power of two <= 1024);
+// lane lc holds, for each block k < V, the four elements 4*L*k + 4*lc + {0..3},
+// so a block of 4L elements is one contiguous, coalesced span per buffer.
+// The chunk's L1 norm is the in-lane (|a0|+|a1|)+(|a2|+|a3|), an xor butterfly
+// over the lanes of a wave (partners l and l^o hold adjacent index ranges),
+// then an in-order tree over the chunk's waves and over its blocks: exactly the
+// balanced pairwise tree over the chunk in index order (the zero padding
+// beyond the chunk length adds +0 and changes no bit).  Packed signs: dword j
+// of a chunk holds elements 32j..32j+31, assembled by an OR butterfly over 8
+// lanes (4 bits per lane) and stored by every 8th lane.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
 #include <type_traits>
 
 #include "zo_internal.h"
 
 namespace zo {
 
+typedef float f4v __attribute__((ext_vector_type(4)));
+
 // ---------------------------------------------------------------------------
-// elementwise helpers
+// streaming access helpers
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ float4 ld4(const float *p, int64_t i4)
+__device__ __forceinline__ f4v ldnt(const float *p, int64_t i4)
 {
-    return reinterpret_cast<const float4 *>(p)[i4];
+    return __builtin_nontemporal_load(reinterpret_cast<const f4v *>(p) + i4);
 }
 
-__device__ __forceinline__ void st4(float *p, int64_t i4, float4 v)
+__device__ __forceinline__ void stnt(float *p, int64_t i4, f4v v)
 {
-    reinterpret_cast<float4 *>(p)[i4] = v;
+    __builtin_nontemporal_store(v, reinterpret_cast<f4v *>(p) + i4);
 }
 
 // Momentum / model / buffer lines of Algorithm 1 for one element, with the
@@ -67,7 +80,7 @@ __device__ __forceinline__ float var_elem(float v, float gb, const Scalars &s)
 }
 
 // ---------------------------------------------------------------------------
-// a1 (+a2): local step, grid-stride over float4
+// a1 (+a2): local step, one float4 per thread
 // ---------------------------------------------------------------------------
 
 template <bool VAR>
@@ -77,24 +90,26 @@ __global__ __launch_bounds__(256) void k_local(const float *__restrict__ g, floa
                                                const float *__restrict__ gbar, int64_t n4,
                                                Scalars s)
 {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-        float4 gg = ld4(g, i), mm = ld4(m, i), xx = ld4(x, i), vv = ld4(v, i), uu = ld4(u, i);
-        local_elem(gg.x, mm.x, xx.x, vv.x, uu.x, s);
-        local_elem(gg.y, mm.y, xx.y, vv.y, uu.y, s);
-        local_elem(gg.z, mm.z, xx.z, vv.z, uu.z, s);
-        local_elem(gg.w, mm.w, xx.w, vv.w, uu.w, s);
-        st4(m, i, mm);
-        st4(x, i, xx);
-        st4(u, i, uu);
-        if (VAR) {
-            float4 gb = ld4(gbar, i);
-            vv.x = var_elem(vv.x, gb.x, s);
-            vv.y = var_elem(vv.y, gb.y, s);
-            vv.z = var_elem(vv.z, gb.z, s);
-            vv.w = var_elem(vv.w, gb.w, s);
-            st4(v, i, vv);
-        }
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n4) return;
+    f4v gg = ldnt(g, i), mm = ldnt(m, i), xx = ldnt(x, i), vv = ldnt(v, i), uu = ldnt(u, i);
+    f4v gb;
+    if (VAR) gb = ldnt(gbar, i);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        float mc = mm[c], xc = xx[c], uc = uu[c];
+        local_elem(gg[c], mc, xc, vv[c], uc, s);
+        mm[c] = mc;
+        xx[c] = xc;
+        uu[c] = uc;
+    }
+    stnt(m, i, mm);
+    stnt(x, i, xx);
+    stnt(u, i, uu);
+    if (VAR) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) vv[c] = var_elem(vv[c], gb[c], s);
+        stnt(v, i, vv);
     }
 }
 
@@ -102,22 +117,19 @@ __global__ __launch_bounds__(256) void k_local(const float *__restrict__ g, floa
 __global__ __launch_bounds__(256) void k_var(float *__restrict__ v, const float *__restrict__ gbar,
                                              int64_t n4, Scalars s)
 {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-        float4 vv = ld4(v, i), gb = ld4(gbar, i);
-        vv.x = var_elem(vv.x, gb.x, s);
-        vv.y = var_elem(vv.y, gb.y, s);
-        vv.z = var_elem(vv.z, gb.z, s);
-        vv.w = var_elem(vv.w, gb.w, s);
-        st4(v, i, vv);
-    }
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n4) return;
+    f4v vv = ldnt(v, i), gb = ldnt(gbar, i);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) vv[c] = var_elem(vv[c], gb[c], s);
+    stnt(v, i, vv);
 }
 
 // ---------------------------------------------------------------------------
 // chunk machinery
 // ---------------------------------------------------------------------------
 
-// Sum over the L lanes of a chunk that share a wave (L <= 64): xor butterfly.
+// Sum over the lanes of a chunk that share a wave: xor butterfly.
 template <int L>
 __device__ __forceinline__ float wave_tree(float x)
 {
@@ -134,9 +146,10 @@ __device__ __forceinline__ uint32_t wave_or8(uint32_t x)
     return x;
 }
 
-// The chunk's pairwise L1 tree, given each lane's per-block partial sums
-// (the in-lane level).  Returns the total to every lane of the chunk.  All
-// threads of the workgroup must call it (it synchronises when L > 64).
+// The chunk's pairwise L1 tree from each lane's per-block partial sums (the
+// in-lane level).  Returns the total to every lane of the chunk.  Every
+// thread of the workgroup must call it (it synchronises when L > 64).  `lds`
+// holds (blockDim / 64) * V floats.
 template <int L, int V>
 __device__ __forceinline__ float chunk_tree(float (&part)[V], float *lds)
 {
@@ -157,31 +170,34 @@ __device__ __forceinline__ float chunk_tree(float (&part)[V], float *lds)
         float bs[V];
 #pragma unroll
         for (int k = 0; k < V; ++k) {
-            if constexpr (NW == 2) {
-                bs[k] = lds[base * V + k] + lds[(base + 1) * V + k];
-            } else {
-                bs[k] = (lds[base * V + k] + lds[(base + 1) * V + k]) +
-                        (lds[(base + 2) * V + k] + lds[(base + 3) * V + k]);
+            float t[NW];
+#pragma unroll
+            for (int w = 0; w < NW; ++w) t[w] = lds[(base + w) * V + k];
+#pragma unroll
+            for (int h = 1; h < NW; h <<= 1) {
+#pragma unroll
+                for (int w = 0; w + h < NW; w += 2 * h) t[w] = t[w] + t[w + h];
             }
+            bs[k] = t[0];
         }
 #pragma unroll
-        for (int w = 1; w < V; w <<= 1) {
+        for (int h = 1; h < V; h <<= 1) {
 #pragma unroll
-            for (int k = 0; k + w < V; k += 2 * w) bs[k] = bs[k] + bs[k + w];
+            for (int k = 0; k + h < V; k += 2 * h) bs[k] = bs[k] + bs[k + h];
         }
         return bs[0];
     }
 }
 
-__device__ __forceinline__ float abs4(float4 a)
+__device__ __forceinline__ float abs4(f4v a)
 {
-    return (fabsf(a.x) + fabsf(a.y)) + (fabsf(a.z) + fabsf(a.w));
+    return (fabsf(a[0]) + fabsf(a[1])) + (fabsf(a[2]) + fabsf(a[3]));
 }
 
-__device__ __forceinline__ uint32_t sign4(float4 a)
+__device__ __forceinline__ uint32_t sign4(f4v a)
 {
-    return (a.x >= 0.0f ? 1u : 0u) | (a.y >= 0.0f ? 2u : 0u) | (a.z >= 0.0f ? 4u : 0u) |
-           (a.w >= 0.0f ? 8u : 0u);
+    return (a[0] >= 0.0f ? 1u : 0u) | (a[1] >= 0.0f ? 2u : 0u) | (a[2] >= 0.0f ? 4u : 0u) |
+           (a[3] >= 0.0f ? 8u : 0u);
 }
 
 __device__ __forceinline__ float ef_elem(float a, float s)
@@ -193,7 +209,7 @@ __device__ __forceinline__ float ef_elem(float a, float s)
 // lanes' registers (zeros beyond `len`): writes the new error, the packed
 // signs (all 2*ceil(len/64) dwords of the chunk) and the scale.
 template <int L, int V>
-__device__ __forceinline__ void compress_chunk(float4 (&a)[V], int lc, int len, bool active,
+__device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, bool active,
                                                float *__restrict__ err, int64_t err_e0,
                                                uint32_t *__restrict__ words32, float *scale_out,
                                                float *lds)
@@ -210,15 +226,13 @@ __device__ __forceinline__ void compress_chunk(float4 (&a)[V], int lc, int len, 
         const bool valid = active && e < len;
         uint32_t nib = 0;
         if (valid) {
-            float4 d;
-            d.x = ef_elem(a[k].x, s);
-            d.y = ef_elem(a[k].y, s);
-            d.z = ef_elem(a[k].z, s);
-            d.w = ef_elem(a[k].w, s);
-            st4(err, (err_e0 + e) >> 2, d);
+            f4v d;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) d[c] = ef_elem(a[k][c], s);
+            stnt(err, (err_e0 + e) >> 2, d);
             nib = sign4(a[k]);
         }
-        uint32_t dw = wave_or8<L>(nib << (4 * (lc & 7)));
+        const uint32_t dw = wave_or8<L>(nib << (4 * (lc & 7)));
         if (active && (lc & 7) == 0) {
             const int j = e >> 5;
             if (j < ndw) words32[j] = dw;
@@ -234,39 +248,33 @@ __device__ __forceinline__ void compress_chunk(float4 (&a)[V], int lc, int len, 
 // ---------------------------------------------------------------------------
 
 template <int L, int V, bool FUSED>
-__global__ __launch_bounds__(256) void k_sync1(const float *__restrict__ g,
-                                               const float *__restrict__ m,
-                                               const float *__restrict__ u,
-                                               float *__restrict__ err, Chunks ch,
-                                               int64_t nchunks, uint32_t *__restrict__ packed32,
-                                               float *__restrict__ scales, Scalars s)
+__global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
+    const float *__restrict__ g, const float *__restrict__ m, const float *__restrict__ u,
+    float *__restrict__ err, Chunks ch, int64_t nchunks, uint32_t *__restrict__ packed32,
+    float *__restrict__ scales, Scalars s)
 {
     __shared__ float lds[64];
-    constexpr int CPW = 256 / L;
+    constexpr int CPW = L >= 256 ? 1 : 256 / L;
     const int lc = threadIdx.x % L;
     const int64_t c = (int64_t)blockIdx.x * CPW + threadIdx.x / L;
     const bool active = c < nchunks;
     const int len = active ? ch.len[c] : 0;
     const int64_t e0 = active ? ch.start[c] : 0;
-    float4 a[V];
+    f4v a[V];
 #pragma unroll
     for (int k = 0; k < V; ++k) {
         const int e = 4 * L * k + 4 * lc;
-        a[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+        a[k] = f4v{0.f, 0.f, 0.f, 0.f};
         if (e < len) {
             const int64_t i4 = (e0 + e) >> 2;
-            float4 uu = ld4(u, i4), dd = ld4(err, i4);
+            f4v uu = ldnt(u, i4), dd = ldnt(err, i4);
             if (FUSED) {
-                float4 gg = ld4(g, i4), mm = ld4(m, i4);
-                uu.x = uu.x + s.gamma * (s.b1 * mm.x + s.c1 * gg.x);
-                uu.y = uu.y + s.gamma * (s.b1 * mm.y + s.c1 * gg.y);
-                uu.z = uu.z + s.gamma * (s.b1 * mm.z + s.c1 * gg.z);
-                uu.w = uu.w + s.gamma * (s.b1 * mm.w + s.c1 * gg.w);
+                const f4v gg = ldnt(g, i4), mm = ldnt(m, i4);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) uu[q] = uu[q] + s.gamma * (s.b1 * mm[q] + s.c1 * gg[q]);
             }
-            a[k].x = uu.x + dd.x;
-            a[k].y = uu.y + dd.y;
-            a[k].z = uu.z + dd.z;
-            a[k].w = uu.w + dd.w;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) a[k][q] = uu[q] + dd[q];
         }
     }
     compress_chunk<L, V>(a, lc, len, active, err, e0, packed32 + 2 * (active ? ch.word[c] : 0),
@@ -319,55 +327,47 @@ __device__ __forceinline__ uint32_t inexact_flag(const float *__restrict__ sc, i
 }
 
 // Plain server: per element, per worker, select +-S_w and add in binary64.
+// Kept for worker counts whose lookup tables do not fit in LDS.
 template <int L, int V>
-__global__ __launch_bounds__(256) void k_srv_plain(const uint32_t *__restrict__ packed32,
-                                                   const float *__restrict__ scales, int W,
-                                                   int64_t wstride, int64_t cstride,
-                                                   Chunks ch, int64_t c0, int64_t nch,
-                                                   int64_t word0, int64_t elem0,
-                                                   float *__restrict__ srv_err,
-                                                   uint32_t *__restrict__ srv_packed32,
-                                                   float *__restrict__ srv_scales,
-                                                   float *__restrict__ avg_out,
-                                                   uint8_t *__restrict__ flags)
+__global__ __launch_bounds__(L > 256 ? L : 256) void k_srv_plain(
+    const uint32_t *__restrict__ packed32, const float *__restrict__ scales, int W,
+    int64_t wstride, int64_t cstride, Chunks ch, int64_t c0, int64_t nch, int64_t word0,
+    int64_t elem0, float *__restrict__ srv_err, uint32_t *__restrict__ srv_packed32,
+    float *__restrict__ srv_scales, float *__restrict__ avg_out, uint8_t *__restrict__ flags,
+    double inv_w, int w_pow2)
 {
     __shared__ float lds[64];
-    constexpr int CPW = 256 / L;
+    constexpr int CPW = L >= 256 ? 1 : 256 / L;
     const int lc = threadIdx.x % L;
     const int64_t cr = (int64_t)blockIdx.x * CPW + threadIdx.x / L;  // chunk within range
     const bool active = cr < nch;
     const int64_t c = c0 + (active ? cr : 0);
     const int len = active ? ch.len[c] : 0;
-    const int64_t el = active ? ch.start[c] - elem0 : 0;      // element offset in range
-    const int64_t wd = active ? ch.word[c] - word0 : 0;       // word offset in range
-    float4 b[V];
+    const int64_t el = active ? ch.start[c] - elem0 : 0;  // element offset in range
+    const int64_t wd = active ? ch.word[c] - word0 : 0;   // word offset in range
+    f4v b[V];
 #pragma unroll
     for (int k = 0; k < V; ++k) {
         const int e = 4 * L * k + 4 * lc;
-        b[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+        b[k] = f4v{0.f, 0.f, 0.f, 0.f};
         if (e < len) {
-            double acc0 = 0.0, acc1 = 0.0, acc2 = 0.0, acc3 = 0.0;
+            double acc[4] = {0.0, 0.0, 0.0, 0.0};
             const int64_t dwi = 2 * wd + (e >> 5);
             const int sh = e & 31;
             for (int w = 0; w < W; ++w) {
                 const uint32_t bits = packed32[2 * wstride * w + dwi] >> sh;
                 const double sw = (double)scales[cstride * w + cr];
-                acc0 += (bits & 1u) ? sw : -sw;
-                acc1 += (bits & 2u) ? sw : -sw;
-                acc2 += (bits & 4u) ? sw : -sw;
-                acc3 += (bits & 8u) ? sw : -sw;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) acc[q] += ((bits >> q) & 1u) ? sw : -sw;
             }
-            float4 av;
-            av.x = (float)(acc0 / (double)W);
-            av.y = (float)(acc1 / (double)W);
-            av.z = (float)(acc2 / (double)W);
-            av.w = (float)(acc3 / (double)W);
-            if (avg_out) st4(avg_out, (el + e) >> 2, av);
-            float4 d = ld4(srv_err, (el + e) >> 2);
-            b[k].x = av.x + d.x;
-            b[k].y = av.y + d.y;
-            b[k].z = av.z + d.z;
-            b[k].w = av.w + d.w;
+            f4v av;
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                av[q] = w_pow2 ? (float)(acc[q] * inv_w) : (float)(acc[q] / (double)W);
+            if (avg_out) stnt(avg_out, (el + e) >> 2, av);
+            const f4v d = ldnt(srv_err, (el + e) >> 2);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) b[k][q] = av[q] + d[q];
         }
     }
     compress_chunk<L, V>(b, lc, len, active, srv_err, el,
@@ -394,7 +394,7 @@ __device__ __forceinline__ void transpose8x32(uint32_t (&x)[8])
         x[k] ^= t << 4;
     }
 #pragma unroll
-    for (int k = 0; k < 8; k += (k & 1) ? 3 : 1) {   // pairs (0,2) (1,3) (4,6) (5,7)
+    for (int k = 0; k < 8; k += (k & 1) ? 3 : 1) {  // pairs (0,2) (1,3) (4,6) (5,7)
         uint32_t t = ((x[k] >> 2) ^ x[k + 2]) & 0x33333333u;
         x[k + 2] ^= t;
         x[k] ^= t << 2;
@@ -422,21 +422,17 @@ __device__ __forceinline__ float tree32_abs(const float (&v)[32])
 }
 
 template <int LD, int R>
-__global__ __launch_bounds__(256) void k_srv_lut(const uint32_t *__restrict__ packed32,
-                                                 const float *__restrict__ scales, int W, int G,
-                                                 int64_t wstride, int64_t cstride, Chunks ch,
-                                                 int64_t c0, int64_t nch, int64_t word0,
-                                                 int64_t elem0, float *__restrict__ srv_err,
-                                                 uint32_t *__restrict__ srv_packed32,
-                                                 float *__restrict__ srv_scales,
-                                                 float *__restrict__ avg_out,
-                                                 uint8_t *__restrict__ flags, int cpw,
-                                                 double inv_w, int w_pow2)
+__global__ __launch_bounds__(LD > 256 ? LD : 256) void k_srv_lut(
+    const uint32_t *__restrict__ packed32, const float *__restrict__ scales, int W, int G,
+    int64_t wstride, int64_t cstride, Chunks ch, int64_t c0, int64_t nch, int64_t word0,
+    int64_t elem0, float *__restrict__ srv_err, uint32_t *__restrict__ srv_packed32,
+    float *__restrict__ srv_scales, float *__restrict__ avg_out, uint8_t *__restrict__ flags,
+    int cpw, double inv_w, int w_pow2)
 {
     extern __shared__ double dyn_lds[];
-    double *tab = dyn_lds;                                   // [cpw][G][256]
+    double *tab = dyn_lds;                                               // [cpw][G][256]
     float *sc = reinterpret_cast<float *>(tab + (size_t)cpw * G * 256);  // [cpw][W]
-    float *tree = sc + (((size_t)cpw * W + 3) & ~(size_t)3); // [64]
+    float *tree = sc + (((size_t)cpw * W + 3) & ~(size_t)3);             // [64]
 
     const int q = threadIdx.x / LD, lc = threadIdx.x % LD;
     const int64_t cbase = (int64_t)blockIdx.x * cpw;
@@ -470,6 +466,7 @@ __global__ __launch_bounds__(256) void k_srv_lut(const uint32_t *__restrict__ pa
     const double *mytab = tab + (size_t)q * G * 256;
 
     const int ndw_data = (len + 31) >> 5;
+    const int64_t ws = 2 * wstride;
     float bv[R][32];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -479,13 +476,20 @@ __global__ __launch_bounds__(256) void k_srv_lut(const uint32_t *__restrict__ pa
         for (int i = 0; i < 32; ++i) acc[i] = 0.0;
         if (j < ndw_data) {
             const uint32_t *src = packed32 + 2 * wd + j;
-            const int64_t ws = 2 * wstride;
+            uint32_t nx[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                nx[k] = (k < W) ? __builtin_nontemporal_load(src + ws * k) : 0u;
             for (int g = 0; g < G; ++g) {
                 uint32_t x[8];
 #pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    const int w = 8 * g + k;
-                    x[k] = (w < W) ? src[ws * w] : 0u;
+                for (int k = 0; k < 8; ++k) x[k] = nx[k];
+                if (g + 1 < G) {  // prefetch the next group while this one is summed
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const int w = 8 * (g + 1) + k;
+                        nx[k] = (w < W) ? __builtin_nontemporal_load(src + ws * w) : 0u;
+                    }
                 }
                 transpose8x32(x);
                 const double *tg = mytab + g * 256;
@@ -500,27 +504,20 @@ __global__ __launch_bounds__(256) void k_srv_lut(const uint32_t *__restrict__ pa
         for (int i4 = 0; i4 < 8; ++i4) {
             const int e = 32 * j + 4 * i4;
             if (e < len) {
-                float4 av;
-                if (w_pow2) {
-                    av.x = (float)(acc[4 * i4 + 0] * inv_w);
-                    av.y = (float)(acc[4 * i4 + 1] * inv_w);
-                    av.z = (float)(acc[4 * i4 + 2] * inv_w);
-                    av.w = (float)(acc[4 * i4 + 3] * inv_w);
-                } else {
-                    av.x = (float)(acc[4 * i4 + 0] / (double)W);
-                    av.y = (float)(acc[4 * i4 + 1] / (double)W);
-                    av.z = (float)(acc[4 * i4 + 2] / (double)W);
-                    av.w = (float)(acc[4 * i4 + 3] / (double)W);
-                }
-                if (avg_out) st4(avg_out, (el + e) >> 2, av);
-                const float4 d = ld4(srv_err, (el + e) >> 2);
-                bv[r][4 * i4 + 0] = av.x + d.x;
-                bv[r][4 * i4 + 1] = av.y + d.y;
-                bv[r][4 * i4 + 2] = av.z + d.z;
-                bv[r][4 * i4 + 3] = av.w + d.w;
+                f4v av;
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq)
+                    av[qq] = w_pow2 ? (float)(acc[4 * i4 + qq] * inv_w)
+                                    : (float)(acc[4 * i4 + qq] / (double)W);
+                // lane-strided accesses (each lane owns 128 contiguous bytes): plain
+                // loads and stores, so that the line stays cached between them
+                if (avg_out) reinterpret_cast<f4v *>(avg_out)[(el + e) >> 2] = av;
+                const f4v d = reinterpret_cast<const f4v *>(srv_err)[(el + e) >> 2];
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) bv[r][4 * i4 + qq] = av[qq] + d[qq];
             } else {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) bv[r][4 * i4 + i] = 0.0f;
+                for (int qq = 0; qq < 4; ++qq) bv[r][4 * i4 + qq] = 0.0f;
             }
         }
     }
@@ -541,14 +538,12 @@ __global__ __launch_bounds__(256) void k_srv_lut(const uint32_t *__restrict__ pa
         for (int i4 = 0; i4 < 8; ++i4) {
             const int e = 32 * j + 4 * i4;
             if (active && e < len) {
-                float4 bb = make_float4(bv[r][4 * i4], bv[r][4 * i4 + 1], bv[r][4 * i4 + 2],
-                                        bv[r][4 * i4 + 3]);
-                float4 d;
-                d.x = ef_elem(bb.x, s);
-                d.y = ef_elem(bb.y, s);
-                d.z = ef_elem(bb.z, s);
-                d.w = ef_elem(bb.w, s);
-                st4(srv_err, (el + e) >> 2, d);
+                const f4v bb = f4v{bv[r][4 * i4], bv[r][4 * i4 + 1], bv[r][4 * i4 + 2],
+                                   bv[r][4 * i4 + 3]};
+                f4v d;
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) d[qq] = ef_elem(bb[qq], s);
+                reinterpret_cast<f4v *>(srv_err)[(el + e) >> 2] = d;
                 bits |= sign4(bb) << (4 * i4);
             }
         }
@@ -562,82 +557,68 @@ __global__ __launch_bounds__(256) void k_srv_lut(const uint32_t *__restrict__ pa
 
 // ---------------------------------------------------------------------------
 // a5 (+a2): reconstruct momentum and model from the server's compressed
-// average; reset the buffer; move the anchor
+// average; reset the buffer; move the anchor.  No reduction, so the grid is
+// cut into 256-thread workgroups over <= 1024-element blocks of one chunk
+// (bpc blocks per chunk) or, for short chunks, several chunks per workgroup
+// (lb lanes per chunk).
 // ---------------------------------------------------------------------------
 
-template <int L, int V, bool VAR>
+template <bool VAR>
 __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_packed32,
                                                const float *__restrict__ srv_scales, Chunks ch,
-                                               int64_t nchunks, float *__restrict__ m,
-                                               float *__restrict__ x, float *__restrict__ v,
-                                               float *__restrict__ u,
+                                               int64_t nchunks, int bpc, int lb,
+                                               float *__restrict__ m, float *__restrict__ x,
+                                               float *__restrict__ v, float *__restrict__ u,
                                                float *__restrict__ anchor,
                                                const float *__restrict__ gbar, float gsum,
                                                Scalars s)
 {
-    constexpr int CPW = 256 / L;
-    const int lc = threadIdx.x % L;
-    const int64_t c = (int64_t)blockIdx.x * CPW + threadIdx.x / L;
+    int64_t c;
+    int e;
+    if (bpc > 1) {
+        c = (int64_t)blockIdx.x / bpc;
+        e = 1024 * (int)(blockIdx.x - c * bpc) + 4 * (int)threadIdx.x;
+    } else {
+        c = (int64_t)blockIdx.x * (256 / lb) + threadIdx.x / lb;
+        e = 4 * (int)(threadIdx.x % lb);
+    }
     if (c >= nchunks) return;
     const int len = ch.len[c];
-    const int64_t e0 = ch.start[c];
+    if (e >= len) return;
+    const int64_t i4 = (ch.start[c] + e) >> 2;
     const float sc = srv_scales[c];
-    const uint32_t *wp = srv_packed32 + 2 * ch.word[c];
+    const uint32_t bits = srv_packed32[2 * ch.word[c] + (e >> 5)] >> (e & 31);
+    const f4v vv = ldnt(v, i4), an = ldnt(anchor, i4);
+    f4v gb;
+    if (VAR) gb = ldnt(gbar, i4);
+    f4v mm, xx, nv;
 #pragma unroll
-    for (int k = 0; k < V; ++k) {
-        const int e = 4 * L * k + 4 * lc;
-        if (e < len) {
-            const int64_t i4 = (e0 + e) >> 2;
-            const uint32_t bits = wp[e >> 5] >> (e & 31);
-            float4 ub;
-            ub.x = (bits & 1u) ? sc : -sc;
-            ub.y = (bits & 2u) ? sc : -sc;
-            ub.z = (bits & 4u) ? sc : -sc;
-            ub.w = (bits & 8u) ? sc : -sc;
-            float4 vv = ld4(v, i4), an = ld4(anchor, i4);
-            float4 mm, xx;
-            mm.x = ub.x / gsum;
-            mm.y = ub.y / gsum;
-            mm.z = ub.z / gsum;
-            mm.w = ub.w / gsum;
-            xx.x = an.x - ub.x / sqrtf(vv.x + s.eps);
-            xx.y = an.y - ub.y / sqrtf(vv.y + s.eps);
-            xx.z = an.z - ub.z / sqrtf(vv.z + s.eps);
-            xx.w = an.w - ub.w / sqrtf(vv.w + s.eps);
-            st4(m, i4, mm);
-            st4(x, i4, xx);
-            st4(anchor, i4, xx);
-            st4(u, i4, make_float4(0.f, 0.f, 0.f, 0.f));
-            if (VAR) {
-                float4 gb = ld4(gbar, i4);
-                vv.x = var_elem(vv.x, gb.x, s);
-                vv.y = var_elem(vv.y, gb.y, s);
-                vv.z = var_elem(vv.z, gb.z, s);
-                vv.w = var_elem(vv.w, gb.w, s);
-                st4(v, i4, vv);
-            }
-        }
+    for (int q = 0; q < 4; ++q) {
+        const float ub = ((bits >> q) & 1u) ? sc : -sc;
+        mm[q] = ub / gsum;
+        xx[q] = an[q] - ub / sqrtf(vv[q] + s.eps);
+        if (VAR) nv[q] = var_elem(vv[q], gb[q], s);
     }
+    stnt(m, i4, mm);
+    stnt(x, i4, xx);
+    stnt(anchor, i4, xx);
+    stnt(u, i4, f4v{0.f, 0.f, 0.f, 0.f});
+    if (VAR) stnt(v, i4, nv);
 }
-
-}  // namespace zo
 
 // ---------------------------------------------------------------------------
 // diagnostic: the division and square root the kernels use
 // ---------------------------------------------------------------------------
-
-namespace zo {
 
 __global__ __launch_bounds__(256) void k_divsqrt(const float *__restrict__ a,
                                                  const float *__restrict__ b,
                                                  float *__restrict__ q, float *__restrict__ r,
                                                  int64_t n)
 {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-        q[i] = a[i] / b[i];
-        r[i] = sqrtf(a[i]);
-    }
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    q[i] = a[i] / b[i];
+    r[i] = sqrtf(a[i]);
 }
 
 // ---------------------------------------------------------------------------
@@ -651,19 +632,19 @@ static inline int next_pow2(int v)
     return p;
 }
 
+// Lanes per chunk and blocks per lane of the compress kernels: one float4 per
+// lane and block, up to 1024 lanes (16 waves) per chunk.
 Geometry geometry_for(int chunk)
 {
     const int lanes = (chunk + 3) / 4;
     if (lanes <= 256) return Geometry{next_pow2(lanes), 1};
-    return Geometry{256, next_pow2((lanes + 255) / 256)};
+    const int L = next_pow2(lanes) < 1024 ? next_pow2(lanes) : 1024;
+    return Geometry{L, next_pow2((lanes + L - 1) / L)};
 }
 
-static inline unsigned stream_grid(int64_t n4)
+static inline unsigned grid_for(int64_t items, int64_t per_block)
 {
-    int64_t blocks = (n4 + 255) / 256;
-    const int64_t cap = 256 * 64;  // 64 workgroups per CU, then grid-stride
-    if (blocks > cap) blocks = cap;
-    return (unsigned)(blocks < 1 ? 1 : blocks);
+    return (unsigned)((items + per_block - 1) / per_block);
 }
 
 // Calls f(integral_constant<L>, integral_constant<V>) for a supported geometry.
@@ -682,18 +663,23 @@ static hipError_t with_geometry(Geometry geo, F &&f)
         case 64: return f(integral_constant<int, 64>{}, integral_constant<int, 1>{});
         case 128: return f(integral_constant<int, 128>{}, integral_constant<int, 1>{});
         case 256: return f(integral_constant<int, 256>{}, integral_constant<int, 1>{});
+        case 512: return f(integral_constant<int, 512>{}, integral_constant<int, 1>{});
+        case 1024: return f(integral_constant<int, 1024>{}, integral_constant<int, 1>{});
         default: return hipErrorInvalidValue;
         }
     }
-    if (geo.L != 256) return hipErrorInvalidValue;
+    if (geo.L != 1024) return hipErrorInvalidValue;
     switch (geo.V) {
-    case 2: return f(integral_constant<int, 256>{}, integral_constant<int, 2>{});
-    case 4: return f(integral_constant<int, 256>{}, integral_constant<int, 4>{});
-    case 8: return f(integral_constant<int, 256>{}, integral_constant<int, 8>{});
-    case 16: return f(integral_constant<int, 256>{}, integral_constant<int, 16>{});
+    case 2: return f(integral_constant<int, 1024>{}, integral_constant<int, 2>{});
+    case 4: return f(integral_constant<int, 1024>{}, integral_constant<int, 4>{});
     default: return hipErrorInvalidValue;
     }
 }
+
+template <int L>
+static inline unsigned chunk_block() { return L > 256 ? L : 256; }
+template <int L>
+static inline int64_t chunks_per_block() { return L >= 256 ? 1 : 256 / L; }
 
 hipError_t launch_local(bool var, const float *g, float *m, float *x, float *v, float *u,
                         const float *gbar, int64_t n, const Scalars &s, hipStream_t st)
@@ -701,11 +687,11 @@ hipError_t launch_local(bool var, const float *g, float *m, float *x, float *v, 
     const int64_t n4 = n / 4;
     if (n4 == 0) return hipSuccess;
     if (var)
-        hipLaunchKernelGGL(k_local<true>, dim3(stream_grid(n4)), dim3(256), 0, st, g, m, x, v, u,
-                           gbar, n4, s);
-    else
-        hipLaunchKernelGGL(k_local<false>, dim3(stream_grid(n4)), dim3(256), 0, st, g, m, x, v,
+        hipLaunchKernelGGL(k_local<true>, dim3(grid_for(n4, 256)), dim3(256), 0, st, g, m, x, v,
                            u, gbar, n4, s);
+    else
+        hipLaunchKernelGGL(k_local<false>, dim3(grid_for(n4, 256)), dim3(256), 0, st, g, m, x,
+                           v, u, gbar, n4, s);
     return hipGetLastError();
 }
 
@@ -713,7 +699,7 @@ hipError_t launch_var(float *v, const float *gbar, int64_t n, const Scalars &s, 
 {
     const int64_t n4 = n / 4;
     if (n4 == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_var, dim3(stream_grid(n4)), dim3(256), 0, st, v, gbar, n4, s);
+    hipLaunchKernelGGL(k_var, dim3(grid_for(n4, 256)), dim3(256), 0, st, v, gbar, n4, s);
     return hipGetLastError();
 }
 
@@ -724,24 +710,25 @@ hipError_t launch_sync1(Geometry geo, bool fused, const float *g, const float *m
     if (nchunks == 0) return hipSuccess;
     return with_geometry(geo, [&](auto Lc, auto Vc) {
         constexpr int L = decltype(Lc)::value, V = decltype(Vc)::value;
-        const unsigned grid = (unsigned)((nchunks + (256 / L) - 1) / (256 / L));
+        const unsigned grid = grid_for(nchunks, chunks_per_block<L>());
         uint32_t *p32 = reinterpret_cast<uint32_t *>(packed);
         if (fused)
-            hipLaunchKernelGGL((k_sync1<L, V, true>), dim3(grid), dim3(256), 0, st, g, m, u, err,
-                               ch, nchunks, p32, scales, s);
+            hipLaunchKernelGGL((k_sync1<L, V, true>), dim3(grid), dim3(chunk_block<L>()), 0, st,
+                               g, m, u, err, ch, nchunks, p32, scales, s);
         else
-            hipLaunchKernelGGL((k_sync1<L, V, false>), dim3(grid), dim3(256), 0, st, g, m, u,
-                               err, ch, nchunks, p32, scales, s);
+            hipLaunchKernelGGL((k_sync1<L, V, false>), dim3(grid), dim3(chunk_block<L>()), 0, st,
+                               g, m, u, err, ch, nchunks, p32, scales, s);
         return hipGetLastError();
     });
 }
 
-// Lanes per chunk and rounds of the LUT server: one lane per packed dword.
+// Lanes per chunk and rounds of the LUT server: one lane per packed dword,
+// up to 512 lanes per chunk.
 static inline Geometry srv_geometry_for(int chunk)
 {
     const int dws = (chunk + 31) / 32;
-    if (dws <= 256) return Geometry{next_pow2(dws), 1};
-    return Geometry{256, next_pow2((dws + 255) / 256)};
+    if (dws <= 512) return Geometry{next_pow2(dws), 1};
+    return Geometry{512, next_pow2((dws + 511) / 512)};
 }
 
 static constexpr size_t kSrvLdsMax = 64 * 1024;
@@ -756,25 +743,26 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
     const int G = (W + 7) / 8;
     const size_t per_chunk = (size_t)G * 256 * 8 + (size_t)W * 4 + 16;
     const Geometry sg = srv_geometry_for(chunk);
+    const bool pow2 = (W & (W - 1)) == 0;
+    const double inv_w = 1.0 / (double)W;
     const bool lut = algo != SRV_PLAIN && sg.V <= 2 && per_chunk + 256 <= kSrvLdsMax;
     if (!lut) {
         return with_geometry(geo, [&](auto Lc, auto Vc) {
             constexpr int L = decltype(Lc)::value, V = decltype(Vc)::value;
-            const unsigned grid = (unsigned)((nch + (256 / L) - 1) / (256 / L));
-            hipLaunchKernelGGL((k_srv_plain<L, V>), dim3(grid), dim3(256), 0, st,
+            hipLaunchKernelGGL((k_srv_plain<L, V>), dim3(grid_for(nch, chunks_per_block<L>())),
+                               dim3(chunk_block<L>()), 0, st,
                                reinterpret_cast<const uint32_t *>(packed), scales, W, wstride,
                                cstride, ch, c0, nch, word0, elem0, srv_err,
-                               reinterpret_cast<uint32_t *>(srv_packed), srv_scales, avg, flags);
+                               reinterpret_cast<uint32_t *>(srv_packed), srv_scales, avg, flags,
+                               inv_w, pow2 ? 1 : 0);
             return hipGetLastError();
         });
     }
-    int cpw = 256 / sg.L;
+    int cpw = sg.L >= 256 ? 1 : 256 / sg.L;
     while (cpw > 1 && (size_t)cpw * per_chunk + 256 > kSrvLdsMax) cpw >>= 1;
-    const size_t lds = (size_t)cpw * ((size_t)G * 256 * 8) + (((size_t)cpw * W + 3) & ~(size_t)3) * 4 +
-                       64 * 4;
-    const bool pow2 = (W & (W - 1)) == 0;
-    const double inv_w = 1.0 / (double)W;
-    const unsigned grid = (unsigned)((nch + cpw - 1) / cpw);
+    const size_t lds = (size_t)cpw * ((size_t)G * 256 * 8) +
+                       (((size_t)cpw * W + 3) & ~(size_t)3) * 4 + 64 * 4;
+    const unsigned grid = grid_for(nch, cpw);
     const unsigned block = (unsigned)(sg.L * cpw);
     auto go = [&](auto Lc, auto Rc) {
         constexpr int L = decltype(Lc)::value, Rr = decltype(Rc)::value;
@@ -786,7 +774,7 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
         return hipGetLastError();
     };
     using std::integral_constant;
-    if (sg.V == 2) return go(integral_constant<int, 256>{}, integral_constant<int, 2>{});
+    if (sg.V == 2) return go(integral_constant<int, 512>{}, integral_constant<int, 2>{});
     switch (sg.L) {
     case 1: return go(integral_constant<int, 1>{}, integral_constant<int, 1>{});
     case 2: return go(integral_constant<int, 2>{}, integral_constant<int, 1>{});
@@ -797,6 +785,7 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
     case 64: return go(integral_constant<int, 64>{}, integral_constant<int, 1>{});
     case 128: return go(integral_constant<int, 128>{}, integral_constant<int, 1>{});
     case 256: return go(integral_constant<int, 256>{}, integral_constant<int, 1>{});
+    case 512: return go(integral_constant<int, 512>{}, integral_constant<int, 1>{});
     default: return hipErrorInvalidValue;
     }
 }
@@ -804,28 +793,37 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
 hipError_t launch_recon(Geometry geo, bool var, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const float *gbar,
-                        float gsum, const Scalars &s, hipStream_t st)
+                        float gsum, const Scalars &s, int chunk, hipStream_t st)
 {
+    (void)geo;
     if (nchunks == 0) return hipSuccess;
-    return with_geometry(geo, [&](auto Lc, auto Vc) {
-        constexpr int L = decltype(Lc)::value, V = decltype(Vc)::value;
-        const unsigned grid = (unsigned)((nchunks + (256 / L) - 1) / (256 / L));
-        const uint32_t *p32 = reinterpret_cast<const uint32_t *>(srv_packed);
-        if (var)
-            hipLaunchKernelGGL((k_recon<L, V, true>), dim3(grid), dim3(256), 0, st, p32,
-                               srv_scales, ch, nchunks, m, x, v, u, anchor, gbar, gsum, s);
-        else
-            hipLaunchKernelGGL((k_recon<L, V, false>), dim3(grid), dim3(256), 0, st, p32,
-                               srv_scales, ch, nchunks, m, x, v, u, anchor, gbar, gsum, s);
-        return hipGetLastError();
-    });
+    const int lanes = (chunk + 3) / 4;
+    int bpc, lb;
+    int64_t grid;
+    if (lanes > 256) {
+        bpc = (lanes + 255) / 256;
+        lb = 256;
+        grid = nchunks * bpc;
+    } else {
+        bpc = 1;
+        lb = next_pow2(lanes);
+        grid = (nchunks + (256 / lb) - 1) / (256 / lb);
+    }
+    const uint32_t *p32 = reinterpret_cast<const uint32_t *>(srv_packed);
+    if (var)
+        hipLaunchKernelGGL(k_recon<true>, dim3((unsigned)grid), dim3(256), 0, st, p32, srv_scales,
+                           ch, nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+    else
+        hipLaunchKernelGGL(k_recon<false>, dim3((unsigned)grid), dim3(256), 0, st, p32,
+                           srv_scales, ch, nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+    return hipGetLastError();
 }
 
 hipError_t launch_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,
                           hipStream_t st)
 {
     if (n <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_divsqrt, dim3(stream_grid((n + 3) / 4)), dim3(256), 0, st, a, b, q, r, n);
+    hipLaunchKernelGGL(k_divsqrt, dim3(grid_for(n, 256)), dim3(256), 0, st, a, b, q, r, n);
     return hipGetLastError();
 }
 
