@@ -18,6 +18,8 @@ duration gives the roofline line.  The CPU baseline times the oracle on a
 bounded contiguous slice of the same shard (rank 0, N = 1 only).
 """
 import argparse
+import csv
+import hashlib
 import json
 import os
 import sys
@@ -27,6 +29,70 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2202_06009_amd", "csrc", "zo_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gpt2-1.5b_hbm_traffic.json")
+COPY_BYTES = 4 << 30          # size of the calibration copies
+# kernel-name prefixes in rocprofv3 output -> bench names; every hot kernel
+# uses one kind of access (nontemporal or plain), calibrated by the matching copy
+KERNEL_KEYS = {"zo::k_local<true>": ("local+var", "nt"), "zo::k_sync1<": ("sync1", "nt"),
+               "zo::k_srv_lut<": ("srv", "plain"), "zo::k_recon<true>": ("recon+var", "nt"),
+               "zo::k_copy<true>": ("copy_nt", None), "zo::k_copy<false>": ("copy_plain", None)}
+
+
+def source_hash():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def summarize_pmc(fetch_dir, write_dir, out_path):
+    """Turn two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over
+    `bench.py --copy-calibration` into per-launch HBM traffic, each counter
+    scaled by what it reads for the calibration copy of COPY_BYTES."""
+    def load(d, counter):
+        vals = {}
+        for root, _, files in os.walk(d):
+            for fn in files:
+                if not fn.endswith("counter_collection.csv"):
+                    continue
+                for r in csv.DictReader(open(os.path.join(root, fn))):
+                    if r["Counter_Name"] != counter:
+                        continue
+                    name = r["Kernel_Name"].replace("void ", "")
+                    for prefix, (key, _) in KERNEL_KEYS.items():
+                        if name.startswith(prefix):
+                            vals.setdefault(key, []).append(float(r["Counter_Value"]))
+        return {k: sum(v) / len(v) for k, v in vals.items()}
+    fetch, write = load(fetch_dir, "FETCH_SIZE"), load(write_dir, "WRITE_SIZE")
+    factors = {kind: {"fetch": COPY_BYTES / (1024.0 * fetch[f"copy_{kind}"]),
+                      "write": COPY_BYTES / (1024.0 * write[f"copy_{kind}"])}
+               for kind in ("nt", "plain")}
+    kernels = {}
+    for prefix, (key, kind) in KERNEL_KEYS.items():
+        if kind is None or key not in fetch or key not in write:
+            continue
+        f, w = factors[kind]["fetch"], factors[kind]["write"]
+        kernels[key] = {"fetch_kib": fetch[key], "write_kib": write[key], "access": kind,
+                        "traffic_bytes": 1024.0 * (fetch[key] * f + write[key] * w)}
+    out = {"source_sha256": source_hash(), "copy_bytes": COPY_BYTES,
+           "copy_kib": {k: {"fetch": fetch[f"copy_{k}"], "write": write[f"copy_{k}"]}
+                        for k in ("nt", "plain")},
+           "factors": factors, "kernels": kernels}
+    with open(out_path, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print(json.dumps(out, indent=1))
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch from the committed counter summary, or None when
+    it is missing or was taken on different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256") != source_hash() or kernel not in t.get("kernels", {}):
+        return None
+    return t["kernels"][kernel]["traffic_bytes"]
 
 
 def algorithmic_bytes(d, nchunks, nwords, W):
@@ -87,9 +153,16 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="gpt2-1.5b")
-    ap.add_argument("--cpu-sample-chunks", type=int, default=512)
+    ap.add_argument("--cpu-sample-chunks", type=int, default=1600)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run plain and nontemporal copies of a known size (for counters)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the HBM traffic summary from two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], TRAFFIC_FILE)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the multi-GPU exchange of the method is not "
               f"part of this build (asked for --gpus {args.gpus})", file=sys.stderr)
@@ -101,6 +174,15 @@ def main():
     from synth import configs as C
 
     zo.lib()
+    if args.copy_calibration:
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for nt in (True, False):
+            for _ in range(3):
+                zo.zo_diag_copy(src, dst, nontemporal=nt)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
     wl = C.get(args.workload)
     d, W = wl.n, wl.world
     dev = torch.device("cuda", 0)
@@ -181,6 +263,8 @@ def main():
                for n in names}
     dom = max(names, key=lambda n: per_kernel[n])
     step_bytes = sum(bytes_.values())
+    tb = measured_traffic(dom)
+    traffic_gb = None if tb is None else round(tb / 1e9, 3)
     out = {
         "metric": "0/1 Adam step params/sec and achieved HBM GB/s (% of peak), 1 MI355X",
         "value": round(value, 1),
@@ -205,7 +289,7 @@ def main():
         "inexact_chunks": inexact,
         "roofline": {"bound": "hbm", "kernel": dom,
                      "achieved": kernels[dom]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": kernels[dom]["frac"], "traffic": None},
+                     "frac": kernels[dom]["frac"], "traffic": traffic_gb},
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)

@@ -221,6 +221,11 @@ const char *zo_last_hip_error(const zo_adam *h);
 int zo_diag_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,
                     hipStream_t stream);
 
+/* Copy float[n] (n a multiple of 4, 16-byte aligned) with the loads and
+ * stores of the streaming kernels: nontemporal != 0 selects nontemporal
+ * accesses.  A reference kernel of known size for HBM byte counters. */
+int zo_diag_copy(const float *src, float *dst, int64_t n, int nontemporal, hipStream_t stream);
+
 /* ---- planning helpers (pure host; usable without a GPU) ----------------- */
 /* Validate a configuration exactly as zo_adam_init does. */
 int zo_config_check(const zo_config *cfg);

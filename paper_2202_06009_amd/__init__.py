@@ -21,7 +21,7 @@ EXPORTS = (
     "zo_compress_pack_ef", "zo_unpack_average", "zo_sync_update", "zo_variance_update",
     "zo_num_chunks", "zo_packed_words", "zo_server_range", "zo_chunk_table", "zo_gamma_sum",
     "zo_next_step", "zo_inexact_chunks", "zo_strerror", "zo_last_hip_error",
-    "zo_diag_divsqrt", "zo_config_check", "zo_plan_num_chunks", "zo_plan_chunks",
+    "zo_diag_divsqrt", "zo_diag_copy", "zo_config_check", "zo_plan_num_chunks", "zo_plan_chunks",
 )
 
 
@@ -80,6 +80,7 @@ def lib():
             "zo_strerror": ([ci], ctypes.c_char_p),
             "zo_last_hip_error": ([vp], ctypes.c_char_p),
             "zo_diag_divsqrt": ([vp, vp, vp, vp, i64, vp], ci),
+            "zo_diag_copy": ([vp, vp, i64, ci, vp], ci),
             "zo_config_check": ([ctypes.POINTER(_Config)], ci),
             "zo_plan_num_chunks": ([i32, vp, i32], i64),
             "zo_plan_chunks": ([i32, vp, i32, vp, vp, vp], i64),
@@ -213,6 +214,13 @@ def zo_diag_divsqrt(a, b, q, r, stream=None):
     rc = lib().zo_diag_divsqrt(_ptr(a), _ptr(b), _ptr(q), _ptr(r), a.numel(), _stream(stream))
     if rc != ZO_OK:
         raise ZoError(rc, "zo_diag_divsqrt")
+
+
+def zo_diag_copy(src, dst, nontemporal=True, stream=None):
+    rc = lib().zo_diag_copy(_ptr(src), _ptr(dst), src.numel(), 1 if nontemporal else 0,
+                            _stream(stream))
+    if rc != ZO_OK:
+        raise ZoError(rc, "zo_diag_copy")
 
 
 class ZoAdam:

@@ -444,4 +444,12 @@ int zo_diag_divsqrt(const float *a, const float *b, float *q, float *r, int64_t 
     return e == hipSuccess ? ZO_OK : ZO_EHIP;
 }
 
+int zo_diag_copy(const float *src, float *dst, int64_t n, int nontemporal, hipStream_t stream)
+{
+    if (n < 0 || n % 4 || (n > 0 && (!src || !dst))) return ZO_EINVAL;
+    if (!aligned(src, 16) || !aligned(dst, 16)) return ZO_EALIGN;
+    hipError_t e = zo::launch_copy(src, dst, n, nontemporal != 0, stream);
+    return e == hipSuccess ? ZO_OK : ZO_EHIP;
+}
+
 }  // extern "C"

@@ -47,6 +47,7 @@ hipError_t launch_recon(Geometry geo, bool var, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const float *gbar,
                         float gsum, const Scalars &s, int chunk, hipStream_t st);
+hipError_t launch_copy(const float *src, float *dst, int64_t n, bool nt, hipStream_t st);
 hipError_t launch_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,
                           hipStream_t st);
 

@@ -385,26 +385,47 @@ __global__ __launch_bounds__(L > 256 ? L : 256) void k_srv_plain(
 // dword per round (round r, lane lc -> dword r*LD + lc of the chunk); the
 // 8 x 32 bit block of a worker group is transposed in registers so that byte c
 // of register k holds element 8c+k's 8 worker bits.
+
+// Swap the bits selected by m << s in x with the bits selected by m in y
+// (a delta swap written as two bit-field inserts).
+__device__ __forceinline__ void swap_bits(uint32_t &x, uint32_t &y, int s, uint32_t m)
+{
+    const uint32_t xs = x >> s, ys = y << s;
+    y = (xs & m) | (y & ~m);
+    x = (ys & (m << s)) | (x & ~(m << s));
+}
+
 __device__ __forceinline__ void transpose8x32(uint32_t (&x)[8])
 {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        uint32_t t = ((x[k] >> 4) ^ x[k + 4]) & 0x0F0F0F0Fu;
-        x[k + 4] ^= t;
-        x[k] ^= t << 4;
-    }
+    for (int k = 0; k < 4; ++k) swap_bits(x[k], x[k + 4], 4, 0x0F0F0F0Fu);
+    swap_bits(x[0], x[2], 2, 0x33333333u);
+    swap_bits(x[1], x[3], 2, 0x33333333u);
+    swap_bits(x[4], x[6], 2, 0x33333333u);
+    swap_bits(x[5], x[7], 2, 0x33333333u);
 #pragma unroll
-    for (int k = 0; k < 8; k += (k & 1) ? 3 : 1) {  // pairs (0,2) (1,3) (4,6) (5,7)
-        uint32_t t = ((x[k] >> 2) ^ x[k + 2]) & 0x33333333u;
-        x[k + 2] ^= t;
-        x[k] ^= t << 2;
-    }
-#pragma unroll
-    for (int k = 0; k < 8; k += 2) {
-        uint32_t t = ((x[k] >> 1) ^ x[k + 1]) & 0x55555555u;
-        x[k + 1] ^= t;
-        x[k] ^= t << 1;
-    }
+    for (int k = 0; k < 8; k += 2) swap_bits(x[k], x[k + 1], 1, 0x55555555u);
+}
+
+// Byte C of x times 8 (a table offset in bytes) in one SDWA instruction.
+template <int C>
+__device__ __forceinline__ uint32_t byte_x8(uint32_t x)
+{
+    uint32_t r;
+    if constexpr (C == 0)
+        asm("v_lshlrev_b32_sdwa %0, 3, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD "
+            "src1_sel:BYTE_0" : "=v"(r) : "v"(x));
+    else if constexpr (C == 1)
+        asm("v_lshlrev_b32_sdwa %0, 3, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD "
+            "src1_sel:BYTE_1" : "=v"(r) : "v"(x));
+    else if constexpr (C == 2)
+        asm("v_lshlrev_b32_sdwa %0, 3, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD "
+            "src1_sel:BYTE_2" : "=v"(r) : "v"(x));
+    else
+        asm("v_lshlrev_b32_sdwa %0, 3, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD "
+            "src1_sel:BYTE_3" : "=v"(r) : "v"(x));
+    __builtin_assume(r < 2048u);  // lets the table base fold into the LDS offset
+    return r;
 }
 
 // In-lane pairwise tree of |v[0..32)| in index order.
@@ -421,21 +442,77 @@ __device__ __forceinline__ float tree32_abs(const float (&v)[32])
     return t[0];
 }
 
-template <int LD, int R>
-__global__ __launch_bounds__(LD > 256 ? LD : 256) void k_srv_lut(
-    const uint32_t *__restrict__ packed32, const float *__restrict__ scales, int W, int G,
+// Load the 8 dwords of worker group g (workers beyond W read as 0).  Plain
+// loads: the nontemporal hint measured no faster for these dword accesses.
+template <int G>
+__device__ __forceinline__ void load_group(uint32_t (&x)[8], const uint32_t *src, int64_t ws, int g,
+                                           int W)
+{
+    if (8 * g + 8 <= W) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) x[k] = src[ws * (8 * g + k)];
+    } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) x[k] = (8 * g + k < W) ? src[ws * (8 * g + k)] : 0u;
+    }
+}
+
+// Worker groups whose packed words are loaded ahead of the one being summed
+// (HBM latency is hidden by bytes in flight, and the table lookups leave
+// registers for only a few groups).
+constexpr int kSrvPrefetch = 2;
+
+// Chunks per workgroup of the LUT server: enough chunks to fill a wave when a
+// chunk has fewer than 64 dwords, as long as their tables fit in 64 KB.
+constexpr int srv_chunks_per_block(int LD, int G)
+{
+    const int fill = LD >= 64 ? 1 : 64 / LD;
+    const int fit = 32 / G > 1 ? 32 / G : 1;
+    return fill < fit ? fill : fit;
+}
+
+// Eight table lookups (byte C of the eight transposed registers) added to
+// their accumulators.  The empty asm consumes the eight sums: the adds, and so
+// the table reads, of one batch complete before the next batch's reads are
+// issued (otherwise the scheduler hoists every read of the unrolled groups and
+// their results, two registers each, spill).
+template <int C>
+__device__ __forceinline__ void lookup8(double (&acc)[32], const uint32_t (&x)[8], const char *tg)
+{
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+        acc[8 * C + k] += *reinterpret_cast<const double *>(tg + byte_x8<C>(x[k]));
+    asm volatile(""
+                 : "+v"(acc[8 * C + 0]), "+v"(acc[8 * C + 1]), "+v"(acc[8 * C + 2]),
+                   "+v"(acc[8 * C + 3]), "+v"(acc[8 * C + 4]), "+v"(acc[8 * C + 5]),
+                   "+v"(acc[8 * C + 6]), "+v"(acc[8 * C + 7])
+                 :
+                 : "memory");
+}
+
+// LD lanes per chunk (one packed dword each per round), R rounds, G groups of
+// 8 workers (a compile-time count; groups past the last worker hold zero
+// tables).  The tables of chunk q of the workgroup start at byte q*G*2048 of
+// `tab`; with one chunk per workgroup the offset of every lookup is an
+// immediate.
+template <int LD, int R, int G>
+__global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
+    const uint32_t *__restrict__ packed32, const float *__restrict__ scales, int W,
     int64_t wstride, int64_t cstride, Chunks ch, int64_t c0, int64_t nch, int64_t word0,
     int64_t elem0, float *__restrict__ srv_err, uint32_t *__restrict__ srv_packed32,
     float *__restrict__ srv_scales, float *__restrict__ avg_out, uint8_t *__restrict__ flags,
-    int cpw, double inv_w, int w_pow2)
+    double inv_w, int w_pow2)
 {
-    extern __shared__ double dyn_lds[];
-    double *tab = dyn_lds;                                               // [cpw][G][256]
-    float *sc = reinterpret_cast<float *>(tab + (size_t)cpw * G * 256);  // [cpw][W]
-    float *tree = sc + (((size_t)cpw * W + 3) & ~(size_t)3);             // [64]
+    constexpr int CPW = srv_chunks_per_block(LD, G);
+    // static arrays: their LDS addresses are link-time constants, so the group
+    // offset of every lookup is an instruction immediate
+    __shared__ double tab[CPW * G * 256];
+    __shared__ float sc[CPW * G * 8];  // W <= 8G
+    __shared__ float tree[64];
 
-    const int q = threadIdx.x / LD, lc = threadIdx.x % LD;
-    const int64_t cbase = (int64_t)blockIdx.x * cpw;
+    const int q = CPW == 1 ? 0 : (int)threadIdx.x / LD;
+    const int lc = CPW == 1 ? (int)threadIdx.x : (int)threadIdx.x % LD;
+    const int64_t cbase = (int64_t)blockIdx.x * CPW;
     const int64_t cr = cbase + q;
     const bool active = cr < nch;
     const int64_t c = c0 + (active ? cr : 0);
@@ -444,12 +521,12 @@ __global__ __launch_bounds__(LD > 256 ? LD : 256) void k_srv_lut(
     const int64_t wd = active ? ch.word[c] - word0 : 0;
 
     // stage the scales of the workgroup's chunks, then build the tables
-    for (int i = threadIdx.x; i < cpw * W; i += blockDim.x) {
+    for (int i = threadIdx.x; i < CPW * W; i += blockDim.x) {
         const int qq = i / W, w = i - qq * W;
         sc[i] = (cbase + qq < nch) ? scales[cstride * w + cbase + qq] : 0.0f;
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < cpw * G * 256; i += blockDim.x) {
+    for (int i = threadIdx.x; i < CPW * G * 256; i += blockDim.x) {
         const int qq = i / (G * 256), g = (i >> 8) % G, b = i & 255;
         double t = 0.0;
 #pragma unroll
@@ -463,9 +540,10 @@ __global__ __launch_bounds__(LD > 256 ? LD : 256) void k_srv_lut(
         tab[i] = t;
     }
     __syncthreads();
-    const double *mytab = tab + (size_t)q * G * 256;
+    const char *mytab = reinterpret_cast<const char *>(tab) + (size_t)q * G * 2048;
 
     const int ndw_data = (len + 31) >> 5;
+    const int ndw = 2 * ((len + 63) >> 6);
     const int64_t ws = 2 * wstride;
     float bv[R][32];
 #pragma unroll
@@ -476,28 +554,21 @@ __global__ __launch_bounds__(LD > 256 ? LD : 256) void k_srv_lut(
         for (int i = 0; i < 32; ++i) acc[i] = 0.0;
         if (j < ndw_data) {
             const uint32_t *src = packed32 + 2 * wd + j;
-            uint32_t nx[8];
+            uint32_t ring[kSrvPrefetch + 1][8];
 #pragma unroll
-            for (int k = 0; k < 8; ++k)
-                nx[k] = (k < W) ? __builtin_nontemporal_load(src + ws * k) : 0u;
+            for (int g = 0; g < kSrvPrefetch && g < G; ++g) load_group<G>(ring[g], src, ws, g, W);
+#pragma unroll
             for (int g = 0; g < G; ++g) {
-                uint32_t x[8];
-#pragma unroll
-                for (int k = 0; k < 8; ++k) x[k] = nx[k];
-                if (g + 1 < G) {  // prefetch the next group while this one is summed
-#pragma unroll
-                    for (int k = 0; k < 8; ++k) {
-                        const int w = 8 * (g + 1) + k;
-                        nx[k] = (w < W) ? __builtin_nontemporal_load(src + ws * w) : 0u;
-                    }
-                }
-                transpose8x32(x);
-                const double *tg = mytab + g * 256;
-#pragma unroll
-                for (int cc = 0; cc < 4; ++cc) {
-#pragma unroll
-                    for (int k = 0; k < 8; ++k) acc[8 * cc + k] += tg[(x[k] >> (8 * cc)) & 0xFFu];
-                }
+                if (g + kSrvPrefetch < G)
+                    load_group<G>(ring[(g + kSrvPrefetch) % (kSrvPrefetch + 1)], src, ws,
+                                  g + kSrvPrefetch, W);
+                uint32_t (&cur)[8] = ring[g % (kSrvPrefetch + 1)];
+                transpose8x32(cur);
+                const char *tg = mytab + g * 2048;
+                lookup8<0>(acc, cur, tg);
+                lookup8<1>(acc, cur, tg);
+                lookup8<2>(acc, cur, tg);
+                lookup8<3>(acc, cur, tg);
             }
         }
 #pragma unroll
@@ -528,7 +599,6 @@ __global__ __launch_bounds__(LD > 256 ? LD : 256) void k_srv_lut(
     for (int r = 0; r < R; ++r) part[r] = tree32_abs(bv[r]);
     const float tot = chunk_tree<LD, R>(part, tree);
     const float s = tot / (float)len;
-    const int ndw = 2 * ((len + 63) >> 6);
     uint32_t *dst = srv_packed32 + 2 * (active ? ch.word[c] : 0);
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -619,6 +689,21 @@ __global__ __launch_bounds__(256) void k_divsqrt(const float *__restrict__ a,
     if (i >= n) return;
     q[i] = a[i] / b[i];
     r[i] = sqrtf(a[i]);
+}
+
+// Plain copy, one float4 per thread, with the same (nontemporal or plain)
+// loads and stores as the streaming kernels: the reference for HBM byte
+// counters.
+template <bool NT>
+__global__ __launch_bounds__(256) void k_copy(const float *__restrict__ src, float *__restrict__ dst,
+                                              int64_t n4)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n4) return;
+    if (NT)
+        stnt(dst, i, ldnt(src, i));
+    else
+        reinterpret_cast<f4v *>(dst)[i] = reinterpret_cast<const f4v *>(src)[i];
 }
 
 // ---------------------------------------------------------------------------
@@ -733,6 +818,40 @@ static inline Geometry srv_geometry_for(int chunk)
 
 static constexpr size_t kSrvLdsMax = 64 * 1024;
 
+template <int LD, int G>
+static hipError_t go_srv_lut(const uint64_t *packed, const float *scales, int W, int64_t wstride,
+                             int64_t cstride, const Chunks &ch, int64_t c0, int64_t nch,
+                             int64_t word0, int64_t elem0, float *srv_err, uint64_t *srv_packed,
+                             float *srv_scales, float *avg, uint8_t *flags, double inv_w,
+                             int pow2, hipStream_t st)
+{
+    constexpr int CPW = srv_chunks_per_block(LD, G);
+    hipLaunchKernelGGL((k_srv_lut<LD, 1, G>), dim3(grid_for(nch, CPW)), dim3(LD * CPW), 0, st,
+                       reinterpret_cast<const uint32_t *>(packed), scales, W, wstride, cstride,
+                       ch, c0, nch, word0, elem0, srv_err, reinterpret_cast<uint32_t *>(srv_packed),
+                       srv_scales, avg, flags, inv_w, pow2);
+    return hipGetLastError();
+}
+
+template <int G>
+static hipError_t srv_lut_ld(int LD, const uint64_t *packed, const float *scales, int W,
+                             int64_t wstride, int64_t cstride, const Chunks &ch, int64_t c0,
+                             int64_t nch, int64_t word0, int64_t elem0, float *srv_err,
+                             uint64_t *srv_packed, float *srv_scales, float *avg, uint8_t *flags,
+                             double inv_w, int pow2, hipStream_t st)
+{
+#define ZO_SRV_LD(L)                                                                           \
+    case L:                                                                                    \
+        return go_srv_lut<L, G>(packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, \
+                                srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    switch (LD) {
+        ZO_SRV_LD(1) ZO_SRV_LD(2) ZO_SRV_LD(4) ZO_SRV_LD(8) ZO_SRV_LD(16) ZO_SRV_LD(32)
+        ZO_SRV_LD(64) ZO_SRV_LD(128) ZO_SRV_LD(256) ZO_SRV_LD(512)
+    default: return hipErrorInvalidValue;
+    }
+#undef ZO_SRV_LD
+}
+
 hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const float *scales, int W,
                       int64_t wstride, int64_t cstride, const Chunks &ch, int64_t c0,
                       int64_t nch, int64_t word0, int64_t elem0, float *srv_err,
@@ -740,12 +859,13 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
                       int chunk, hipStream_t st)
 {
     if (nch == 0) return hipSuccess;
-    const int G = (W + 7) / 8;
-    const size_t per_chunk = (size_t)G * 256 * 8 + (size_t)W * 4 + 16;
     const Geometry sg = srv_geometry_for(chunk);
+    const int G = next_pow2((W + 7) / 8);
+    const int cpw = srv_chunks_per_block(sg.L, G);
+    const size_t lds = (size_t)cpw * G * 2048 + (size_t)cpw * G * 32 + 256;
     const bool pow2 = (W & (W - 1)) == 0;
     const double inv_w = 1.0 / (double)W;
-    const bool lut = algo != SRV_PLAIN && sg.V <= 2 && per_chunk + 256 <= kSrvLdsMax;
+    const bool lut = algo != SRV_PLAIN && sg.V == 1 && G <= 16 && lds <= kSrvLdsMax;
     if (!lut) {
         return with_geometry(geo, [&](auto Lc, auto Vc) {
             constexpr int L = decltype(Lc)::value, V = decltype(Vc)::value;
@@ -758,34 +878,12 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
             return hipGetLastError();
         });
     }
-    int cpw = sg.L >= 256 ? 1 : 256 / sg.L;
-    while (cpw > 1 && (size_t)cpw * per_chunk + 256 > kSrvLdsMax) cpw >>= 1;
-    const size_t lds = (size_t)cpw * ((size_t)G * 256 * 8) +
-                       (((size_t)cpw * W + 3) & ~(size_t)3) * 4 + 64 * 4;
-    const unsigned grid = grid_for(nch, cpw);
-    const unsigned block = (unsigned)(sg.L * cpw);
-    auto go = [&](auto Lc, auto Rc) {
-        constexpr int L = decltype(Lc)::value, Rr = decltype(Rc)::value;
-        hipLaunchKernelGGL((k_srv_lut<L, Rr>), dim3(grid), dim3(block), lds, st,
-                           reinterpret_cast<const uint32_t *>(packed), scales, W, G, wstride,
-                           cstride, ch, c0, nch, word0, elem0, srv_err,
-                           reinterpret_cast<uint32_t *>(srv_packed), srv_scales, avg, flags, cpw,
-                           inv_w, pow2 ? 1 : 0);
-        return hipGetLastError();
-    };
-    using std::integral_constant;
-    if (sg.V == 2) return go(integral_constant<int, 512>{}, integral_constant<int, 2>{});
-    switch (sg.L) {
-    case 1: return go(integral_constant<int, 1>{}, integral_constant<int, 1>{});
-    case 2: return go(integral_constant<int, 2>{}, integral_constant<int, 1>{});
-    case 4: return go(integral_constant<int, 4>{}, integral_constant<int, 1>{});
-    case 8: return go(integral_constant<int, 8>{}, integral_constant<int, 1>{});
-    case 16: return go(integral_constant<int, 16>{}, integral_constant<int, 1>{});
-    case 32: return go(integral_constant<int, 32>{}, integral_constant<int, 1>{});
-    case 64: return go(integral_constant<int, 64>{}, integral_constant<int, 1>{});
-    case 128: return go(integral_constant<int, 128>{}, integral_constant<int, 1>{});
-    case 256: return go(integral_constant<int, 256>{}, integral_constant<int, 1>{});
-    case 512: return go(integral_constant<int, 512>{}, integral_constant<int, 1>{});
+    switch (G) {
+    case 1: return srv_lut_ld<1>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 2: return srv_lut_ld<2>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 4: return srv_lut_ld<4>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 8: return srv_lut_ld<8>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 16: return srv_lut_ld<16>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
     default: return hipErrorInvalidValue;
     }
 }
@@ -816,6 +914,17 @@ hipError_t launch_recon(Geometry geo, bool var, const uint64_t *srv_packed,
     else
         hipLaunchKernelGGL(k_recon<false>, dim3((unsigned)grid), dim3(256), 0, st, p32,
                            srv_scales, ch, nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy(const float *src, float *dst, int64_t n, bool nt, hipStream_t st)
+{
+    const int64_t n4 = n / 4;
+    if (n4 == 0) return hipSuccess;
+    if (nt)
+        hipLaunchKernelGGL(k_copy<true>, dim3(grid_for(n4, 256)), dim3(256), 0, st, src, dst, n4);
+    else
+        hipLaunchKernelGGL(k_copy<false>, dim3(grid_for(n4, 256)), dim3(256), 0, st, src, dst, n4);
     return hipGetLastError();
 }
 
