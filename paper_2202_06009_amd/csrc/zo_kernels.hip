@@ -156,6 +156,12 @@ __device__ __forceinline__ float chunk_tree(float (&part)[V], float *lds)
 #pragma unroll
     for (int k = 0; k < V; ++k) part[k] = wave_tree<L>(part[k]);
     if constexpr (L <= 64) {
+        // the chunk's lanes share a wave: the in-order tree over its blocks
+#pragma unroll
+        for (int h = 1; h < V; h <<= 1) {
+#pragma unroll
+            for (int k = 0; k + h < V; k += 2 * h) part[k] = part[k] + part[k + h];
+        }
         return part[0];
     } else {
         constexpr int NW = L / 64;  // waves per chunk
@@ -220,6 +226,7 @@ __device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, boo
     const float tot = chunk_tree<L, V>(part, lds);
     const float s = tot / (float)len;
     const int ndw = 2 * ((len + 63) >> 6);
+    uint32_t pend = 0;  // L < 8: several blocks share a dword
 #pragma unroll
     for (int k = 0; k < V; ++k) {
         const int e = 4 * L * k + 4 * lc;
@@ -233,12 +240,24 @@ __device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, boo
             nib = sign4(a[k]);
         }
         const uint32_t dw = wave_or8<L>(nib << (4 * (lc & 7)));
-        if (active && (lc & 7) == 0) {
-            const int j = e >> 5;
-            if (j < ndw) words32[j] = dw;
-            if (L <= 8 && ndw > 1) words32[1] = 0u;
+        if constexpr (L >= 8) {
+            // lanes 8q..8q+7 hold dword 4Lk/32 + q
+            if (active && (lc & 7) == 0) {
+                const int j = e >> 5;
+                if (j < ndw) words32[j] = dw;
+            }
+        } else {
+            pend |= dw << ((4 * L * k) & 31);
+            if (((4 * L * (k + 1)) & 31) == 0 || k == V - 1) {
+                const int j = (4 * L * k) >> 5;
+                if (active && lc == 0 && j < ndw) words32[j] = pend;
+                pend = 0;
+            }
         }
     }
+    // the chunk's last word may hold a dword of pad bits only, past the lanes
+    constexpr int kCovered = (4 * L * V + 31) / 32;
+    if (active && lc == 0 && kCovered < ndw) words32[kCovered] = 0u;
     if (active && lc == 0) *scale_out = s;
 }
 
@@ -428,20 +447,6 @@ __device__ __forceinline__ uint32_t byte_x8(uint32_t x)
     return r;
 }
 
-// In-lane pairwise tree of |v[0..32)| in index order.
-__device__ __forceinline__ float tree32_abs(const float (&v)[32])
-{
-    float t[32];
-#pragma unroll
-    for (int i = 0; i < 32; ++i) t[i] = fabsf(v[i]);
-#pragma unroll
-    for (int w = 1; w < 32; w <<= 1) {
-#pragma unroll
-        for (int i = 0; i + w < 32; i += 2 * w) t[i] = t[i] + t[i + w];
-    }
-    return t[0];
-}
-
 // Load the 8 dwords of worker group g (workers beyond W read as 0).  Plain
 // loads: the nontemporal hint measured no faster for these dword accesses.
 template <int G>
@@ -490,12 +495,21 @@ __device__ __forceinline__ void lookup8(double (&acc)[32], const uint32_t (&x)[8
                  : "memory");
 }
 
-// LD lanes per chunk (one packed dword each per round), R rounds, G groups of
-// 8 workers (a compile-time count; groups past the last worker hold zero
-// tables).  The tables of chunk q of the workgroup start at byte q*G*2048 of
+// LD lanes per chunk (one packed dword each), G groups of 8 workers (a
+// compile-time count; groups past the last worker hold zero tables).  The tables of chunk q of the workgroup start at byte q*G*2048 of
 // `tab`; with one chunk per workgroup the offset of every lookup is an
 // immediate.
-template <int LD, int R, int G>
+// Float4 slot of the transpose buffer that holds float4 t of a chunk (t = e/4).
+// Lane j writes the slots 8j..8j+7 of its dword; lanes then read slots in
+// coalesced order.  XOR-ing the slot's low three bits with bits 1..3 of j makes
+// both the writes and the reads of 16 consecutive lanes hit 16 distinct
+// 16-byte bank groups.
+__device__ __forceinline__ int xpose_slot(int t)
+{
+    return 8 * (t >> 3) + ((t & 7) ^ ((t >> 4) & 7));
+}
+
+template <int LD, int G>
 __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
     const uint32_t *__restrict__ packed32, const float *__restrict__ scales, int W,
     int64_t wstride, int64_t cstride, Chunks ch, int64_t c0, int64_t nch, int64_t word0,
@@ -505,10 +519,14 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
 {
     constexpr int CPW = srv_chunks_per_block(LD, G);
     // static arrays: their LDS addresses are link-time constants, so the group
-    // offset of every lookup is an instruction immediate
-    __shared__ double tab[CPW * G * 256];
+    // offset of every lookup is an instruction immediate.  The tables are dead
+    // once the sums are formed; the same memory then transposes the averages.
+    constexpr int kTabBytes = CPW * G * 256 * 8;
+    constexpr int kXposeBytes = CPW * LD * 32 * 4;
+    __shared__ double uni[(kTabBytes > kXposeBytes ? kTabBytes : kXposeBytes) / 8];
     __shared__ float sc[CPW * G * 8];  // W <= 8G
     __shared__ float tree[64];
+    double *tab = uni;
 
     const int q = CPW == 1 ? 0 : (int)threadIdx.x / LD;
     const int lc = CPW == 1 ? (int)threadIdx.x : (int)threadIdx.x % LD;
@@ -542,85 +560,61 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
     __syncthreads();
     const char *mytab = reinterpret_cast<const char *>(tab) + (size_t)q * G * 2048;
 
+    // the sum over workers of the lane's 32 elements (dword lc of the chunk)
     const int ndw_data = (len + 31) >> 5;
-    const int ndw = 2 * ((len + 63) >> 6);
     const int64_t ws = 2 * wstride;
-    float bv[R][32];
+    double acc[32];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int j = r * LD + lc;
-        double acc[32];
+    for (int i = 0; i < 32; ++i) acc[i] = 0.0;
+    if (lc < ndw_data) {
+        const uint32_t *src = packed32 + 2 * wd + lc;
+        uint32_t ring[kSrvPrefetch + 1][8];
 #pragma unroll
-        for (int i = 0; i < 32; ++i) acc[i] = 0.0;
-        if (j < ndw_data) {
-            const uint32_t *src = packed32 + 2 * wd + j;
-            uint32_t ring[kSrvPrefetch + 1][8];
+        for (int g = 0; g < kSrvPrefetch && g < G; ++g) load_group<G>(ring[g], src, ws, g, W);
 #pragma unroll
-            for (int g = 0; g < kSrvPrefetch && g < G; ++g) load_group<G>(ring[g], src, ws, g, W);
-#pragma unroll
-            for (int g = 0; g < G; ++g) {
-                if (g + kSrvPrefetch < G)
-                    load_group<G>(ring[(g + kSrvPrefetch) % (kSrvPrefetch + 1)], src, ws,
-                                  g + kSrvPrefetch, W);
-                uint32_t (&cur)[8] = ring[g % (kSrvPrefetch + 1)];
-                transpose8x32(cur);
-                const char *tg = mytab + g * 2048;
-                lookup8<0>(acc, cur, tg);
-                lookup8<1>(acc, cur, tg);
-                lookup8<2>(acc, cur, tg);
-                lookup8<3>(acc, cur, tg);
-            }
-        }
-#pragma unroll
-        for (int i4 = 0; i4 < 8; ++i4) {
-            const int e = 32 * j + 4 * i4;
-            if (e < len) {
-                f4v av;
-#pragma unroll
-                for (int qq = 0; qq < 4; ++qq)
-                    av[qq] = w_pow2 ? (float)(acc[4 * i4 + qq] * inv_w)
-                                    : (float)(acc[4 * i4 + qq] / (double)W);
-                // lane-strided accesses (each lane owns 128 contiguous bytes): plain
-                // loads and stores, so that the line stays cached between them
-                if (avg_out) reinterpret_cast<f4v *>(avg_out)[(el + e) >> 2] = av;
-                const f4v d = reinterpret_cast<const f4v *>(srv_err)[(el + e) >> 2];
-#pragma unroll
-                for (int qq = 0; qq < 4; ++qq) bv[r][4 * i4 + qq] = av[qq] + d[qq];
-            } else {
-#pragma unroll
-                for (int qq = 0; qq < 4; ++qq) bv[r][4 * i4 + qq] = 0.0f;
-            }
+        for (int g = 0; g < G; ++g) {
+            if (g + kSrvPrefetch < G)
+                load_group<G>(ring[(g + kSrvPrefetch) % (kSrvPrefetch + 1)], src, ws,
+                              g + kSrvPrefetch, W);
+            uint32_t (&cur)[8] = ring[g % (kSrvPrefetch + 1)];
+            transpose8x32(cur);
+            const char *tg = mytab + g * 2048;
+            lookup8<0>(acc, cur, tg);
+            lookup8<1>(acc, cur, tg);
+            lookup8<2>(acc, cur, tg);
+            lookup8<3>(acc, cur, tg);
         }
     }
 
-    // Equation 3 with the server error, in the same lane layout
-    float part[R];
+    // averages -> LDS, then back in the coalesced layout of the compress step
+    // (lane lc holds the float4s lc + LD*k, k < 8, of its chunk)
+    __syncthreads();  // every lookup is done: the tables may be overwritten
+    f4v *xp = reinterpret_cast<f4v *>(uni) + (size_t)q * LD * 8;
 #pragma unroll
-    for (int r = 0; r < R; ++r) part[r] = tree32_abs(bv[r]);
-    const float tot = chunk_tree<LD, R>(part, tree);
-    const float s = tot / (float)len;
-    uint32_t *dst = srv_packed32 + 2 * (active ? ch.word[c] : 0);
+    for (int p = 0; p < 8; ++p) {
+        f4v av;
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-        const int j = r * LD + lc;
-        uint32_t bits = 0;
-#pragma unroll
-        for (int i4 = 0; i4 < 8; ++i4) {
-            const int e = 32 * j + 4 * i4;
-            if (active && e < len) {
-                const f4v bb = f4v{bv[r][4 * i4], bv[r][4 * i4 + 1], bv[r][4 * i4 + 2],
-                                   bv[r][4 * i4 + 3]};
-                f4v d;
-#pragma unroll
-                for (int qq = 0; qq < 4; ++qq) d[qq] = ef_elem(bb[qq], s);
-                reinterpret_cast<f4v *>(srv_err)[(el + e) >> 2] = d;
-                bits |= sign4(bb) << (4 * i4);
-            }
-        }
-        if (active && j < ndw) dst[j] = bits;
+        for (int qq = 0; qq < 4; ++qq)
+            av[qq] = w_pow2 ? (float)(acc[4 * p + qq] * inv_w) : (float)(acc[4 * p + qq] / (double)W);
+        xp[xpose_slot(8 * lc + p)] = av;
     }
-    if (LD * R == 1 && active && ndw > 1) dst[1] = 0u;
-    if (active && lc == 0) srv_scales[c] = s;
+    __syncthreads();
+    f4v bv[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const int e = 4 * LD * k + 4 * lc;
+        bv[k] = f4v{0.f, 0.f, 0.f, 0.f};
+        if (e < len) {
+            const f4v av = xp[xpose_slot(LD * k + lc)];
+            if (avg_out) stnt(avg_out, (el + e) >> 2, av);
+            const f4v d = ldnt(srv_err, (el + e) >> 2);
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) bv[k][qq] = av[qq] + d[qq];
+        }
+    }
+    // Equation 3 with the server error
+    compress_chunk<LD, 8>(bv, lc, len, active, srv_err, el,
+                          srv_packed32 + 2 * (active ? ch.word[c] : 0), srv_scales + c, tree);
     const uint32_t f = inexact_flag<LD>(scales + (active ? cr : 0), cstride, W, lc);
     if (active && lc == 0) flags[cr] = (uint8_t)f;
 }
@@ -816,7 +810,7 @@ static inline Geometry srv_geometry_for(int chunk)
     return Geometry{512, next_pow2((dws + 511) / 512)};
 }
 
-static constexpr size_t kSrvLdsMax = 64 * 1024;
+static constexpr size_t kSrvLdsMax = 96 * 1024;
 
 template <int LD, int G>
 static hipError_t go_srv_lut(const uint64_t *packed, const float *scales, int W, int64_t wstride,
@@ -826,7 +820,7 @@ static hipError_t go_srv_lut(const uint64_t *packed, const float *scales, int W,
                              int pow2, hipStream_t st)
 {
     constexpr int CPW = srv_chunks_per_block(LD, G);
-    hipLaunchKernelGGL((k_srv_lut<LD, 1, G>), dim3(grid_for(nch, CPW)), dim3(LD * CPW), 0, st,
+    hipLaunchKernelGGL((k_srv_lut<LD, G>), dim3(grid_for(nch, CPW)), dim3(LD * CPW), 0, st,
                        reinterpret_cast<const uint32_t *>(packed), scales, W, wstride, cstride,
                        ch, c0, nch, word0, elem0, srv_err, reinterpret_cast<uint32_t *>(srv_packed),
                        srv_scales, avg, flags, inv_w, pow2);
@@ -862,7 +856,8 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
     const Geometry sg = srv_geometry_for(chunk);
     const int G = next_pow2((W + 7) / 8);
     const int cpw = srv_chunks_per_block(sg.L, G);
-    const size_t lds = (size_t)cpw * G * 2048 + (size_t)cpw * G * 32 + 256;
+    const size_t tab = (size_t)cpw * G * 2048, xpose = (size_t)cpw * sg.L * 128;
+    const size_t lds = (tab > xpose ? tab : xpose) + (size_t)cpw * G * 32 + 256;
     const bool pow2 = (W & (W - 1)) == 0;
     const double inv_w = 1.0 / (double)W;
     const bool lut = algo != SRV_PLAIN && sg.V == 1 && G <= 16 && lds <= kSrvLdsMax;
