@@ -449,16 +449,32 @@ __device__ __forceinline__ uint32_t byte_x8(uint32_t x)
 
 // Load the 8 dwords of worker group g (workers beyond W read as 0).  Plain
 // loads: the nontemporal hint measured no faster for these dword accesses.
-template <int G>
-__device__ __forceinline__ void load_group(uint32_t (&x)[8], const uint32_t *src, int64_t ws, int g,
-                                           int W)
+// a value the whole wave agrees on, moved to scalar registers: a load at
+// p + wave_uniform(off) + lane is then addressed as scalar base + lane offset
+__device__ __forceinline__ int64_t wave_uniform(int64_t v)
 {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Dword lc of the chunk for the 8 workers of group g: worker w's words start
+// at dword off + ws*w.  UNIFORM: the whole wave is on one chunk, so the row
+// offsets are scalars and each load costs one address add.
+template <bool UNIFORM>
+__device__ __forceinline__ void load_group(uint32_t (&x)[8], const uint32_t *packed32, int64_t off,
+                                           int64_t ws, int g, int W, uint32_t lc)
+{
+    int64_t r[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+        r[k] = UNIFORM ? wave_uniform(off + ws * (8 * g + k)) : off + ws * (8 * g + k);
     if (8 * g + 8 <= W) {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) x[k] = src[ws * (8 * g + k)];
+        for (int k = 0; k < 8; ++k) x[k] = packed32[r[k] + lc];
     } else {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) x[k] = (8 * g + k < W) ? src[ws * (8 * g + k)] : 0u;
+        for (int k = 0; k < 8; ++k) x[k] = 8 * g + k < W ? packed32[r[k] + lc] : 0u;
     }
 }
 
@@ -525,6 +541,7 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
     constexpr int kXposeBytes = CPW * LD * 32 * 4;
     __shared__ double uni[(kTabBytes > kXposeBytes ? kTabBytes : kXposeBytes) / 8];
     __shared__ float sc[CPW * G * 8];  // W <= 8G
+    __shared__ double half[CPW * G * 32];  // per group: 16 sums of workers 0-3, 16 of 4-7
     __shared__ float tree[64];
     double *tab = uni;
 
@@ -538,56 +555,87 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
     const int64_t el = active ? ch.start[c] - elem0 : 0;
     const int64_t wd = active ? ch.word[c] - word0 : 0;
 
+    // lane lc sums the 32 elements of dword lc of the chunk, if the chunk has it
+    const int ndw_data = (len + 31) >> 5;
+    const bool has_dw = lc < ndw_data;
+    const int64_t ws = 2 * wstride;
+    const int64_t off = 2 * wd;
+    constexpr bool kUni = LD >= 64;  // a wave never spans two chunks
+    uint32_t ring[kSrvPrefetch + 1][8];
+
     // stage the scales of the workgroup's chunks, then build the tables
     for (int i = threadIdx.x; i < CPW * W; i += blockDim.x) {
         const int qq = i / W, w = i - qq * W;
         sc[i] = (cbase + qq < nch) ? scales[cstride * w + cbase + qq] : 0.0f;
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < CPW * G * 256; i += blockDim.x) {
-        const int qq = i / (G * 256), g = (i >> 8) % G, b = i & 255;
+    // T_g[b] = H_g,0[b & 15] + H_g,1[b >> 4], with H_g,h[n] the signed sum of
+    // workers 8g+4h .. 8g+4h+3 (every partial sum is exact, so the split is
+    // too)
+    for (int i = threadIdx.x; i < CPW * G * 32; i += blockDim.x) {
+        const int qq = i / (G * 32), g = (i >> 5) % G, h = (i >> 4) & 1, nb = i & 15;
         double t = 0.0;
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int w = 8 * g + k;
+        for (int k = 0; k < 4; ++k) {
+            const int w = 8 * g + 4 * h + k;
             if (w < W) {
                 const double sw = (double)sc[qq * W + w];
-                t += ((b >> k) & 1) ? sw : -sw;
+                t += ((nb >> k) & 1) ? sw : -sw;
             }
         }
-        tab[i] = t;
+        half[i] = t;
+    }
+    {
+        const uint32_t f = inexact_flag<LD>(sc + q * W, 1, W, lc);
+        if (active && lc == 0) flags[cr] = (uint8_t)f;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < CPW * G * 256; i += blockDim.x) {
+        const int qg = i >> 8, b = i & 255;  // qg = chunk * G + group
+        tab[i] = half[32 * qg + (b & 15)] + half[32 * qg + 16 + (b >> 4)];
     }
     __syncthreads();
     const char *mytab = reinterpret_cast<const char *>(tab) + (size_t)q * G * 2048;
 
-    // the sum over workers of the lane's 32 elements (dword lc of the chunk)
-    const int ndw_data = (len + 31) >> 5;
-    const int64_t ws = 2 * wstride;
+    // the server error of the lane's elements in the compress layout (lane lc
+    // holds the float4s lc + LD*k, k < 8, of its chunk); loaded while the last
+    // group's lookups run
+    f4v serr[8];
+    auto load_serr = [&]() {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int e = 4 * LD * k + 4 * lc;
+            serr[k] = e < len ? ldnt(srv_err, (el + e) >> 2) : f4v{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+
+    // the sum over workers of the lane's 32 elements
     double acc[32];
 #pragma unroll
     for (int i = 0; i < 32; ++i) acc[i] = 0.0;
-    if (lc < ndw_data) {
-        const uint32_t *src = packed32 + 2 * wd + lc;
-        uint32_t ring[kSrvPrefetch + 1][8];
+    if (has_dw) {
 #pragma unroll
-        for (int g = 0; g < kSrvPrefetch && g < G; ++g) load_group<G>(ring[g], src, ws, g, W);
+        for (int g = 0; g < kSrvPrefetch && g < G; ++g)
+            load_group<kUni>(ring[g], packed32, off, ws, g, W, lc);
 #pragma unroll
         for (int g = 0; g < G; ++g) {
             if (g + kSrvPrefetch < G)
-                load_group<G>(ring[(g + kSrvPrefetch) % (kSrvPrefetch + 1)], src, ws,
-                              g + kSrvPrefetch, W);
+                load_group<kUni>(ring[(g + kSrvPrefetch) % (kSrvPrefetch + 1)], packed32, off,
+                                 ws, g + kSrvPrefetch, W, lc);
             uint32_t (&cur)[8] = ring[g % (kSrvPrefetch + 1)];
             transpose8x32(cur);
             const char *tg = mytab + g * 2048;
             lookup8<0>(acc, cur, tg);
             lookup8<1>(acc, cur, tg);
             lookup8<2>(acc, cur, tg);
+            if (g == G - 1) load_serr();
             lookup8<3>(acc, cur, tg);
         }
+    } else {
+        load_serr();
     }
 
     // averages -> LDS, then back in the coalesced layout of the compress step
-    // (lane lc holds the float4s lc + LD*k, k < 8, of its chunk)
     __syncthreads();  // every lookup is done: the tables may be overwritten
     f4v *xp = reinterpret_cast<f4v *>(uni) + (size_t)q * LD * 8;
 #pragma unroll
@@ -607,16 +655,13 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
         if (e < len) {
             const f4v av = xp[xpose_slot(LD * k + lc)];
             if (avg_out) stnt(avg_out, (el + e) >> 2, av);
-            const f4v d = ldnt(srv_err, (el + e) >> 2);
 #pragma unroll
-            for (int qq = 0; qq < 4; ++qq) bv[k][qq] = av[qq] + d[qq];
+            for (int qq = 0; qq < 4; ++qq) bv[k][qq] = av[qq] + serr[k][qq];
         }
     }
     // Equation 3 with the server error
     compress_chunk<LD, 8>(bv, lc, len, active, srv_err, el,
                           srv_packed32 + 2 * (active ? ch.word[c] : 0), srv_scales + c, tree);
-    const uint32_t f = inexact_flag<LD>(scales + (active ? cr : 0), cstride, W, lc);
-    if (active && lc == 0) flags[cr] = (uint8_t)f;
 }
 
 // ---------------------------------------------------------------------------
@@ -857,7 +902,7 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
     const int G = next_pow2((W + 7) / 8);
     const int cpw = srv_chunks_per_block(sg.L, G);
     const size_t tab = (size_t)cpw * G * 2048, xpose = (size_t)cpw * sg.L * 128;
-    const size_t lds = (tab > xpose ? tab : xpose) + (size_t)cpw * G * 32 + 256;
+    const size_t lds = (tab > xpose ? tab : xpose) + (size_t)cpw * G * 32 + (size_t)cpw * G * 256 + 256;
     const bool pow2 = (W & (W - 1)) == 0;
     const double inv_w = 1.0 / (double)W;
     const bool lut = algo != SRV_PLAIN && sg.V == 1 && G <= 16 && lds <= kSrvLdsMax;
