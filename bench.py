@@ -8,6 +8,10 @@ optimizer steps that together run every kernel of the path once:
   step 2k+1 (sync, variance update):   K_sync1             (zo_compress_pack_ef)
                                        K_srv, W = 128      (zo_unpack_average)
                                        K_recon+var         (zo_sync_update)
+The reconstruction defers its x and u writes (the new model stays in the
+anchor buffer, u is an implicit zero that the next local step does not read;
+same values, 12 bytes per parameter less per bench step); --eager-sync-writes
+times the eager variant.
 Inputs (gradient, averaged gradient, peers' packed signs and scales) are
 generated once on the device before timing and stay resident in HBM.
 `value` is optimizer-step parameter updates per second (2 d per bench step).
@@ -33,10 +37,14 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2202_06009_amd", "csrc", "zo_kernels.h
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gpt2-1.5b_hbm_traffic.json")
 COPY_BYTES = 4 << 30          # size of the calibration copies
 # kernel-name prefixes in rocprofv3 output -> bench names; every hot kernel
-# uses one kind of access (nontemporal or plain), calibrated by the matching copy
-KERNEL_KEYS = {"zo::k_local<true>": ("local+var", "nt"), "zo::k_sync1<": ("sync1", "nt"),
-               "zo::k_srv_lut<": ("srv", "plain"), "zo::k_recon<true>": ("recon+var", "nt"),
-               "zo::k_copy<true>": ("copy_nt", None), "zo::k_copy<false>": ("copy_plain", None)}
+# uses one kind of access (nontemporal or plain), calibrated by the matching copy.
+# The second template argument of k_local / k_recon is the deferred variant
+# (the very first local step of a run has no sync before it and is skipped).
+def kernel_keys(sync_writes):
+    dv = "true" if sync_writes == "deferred" else "false"
+    return {f"zo::k_local<true, {dv}>": ("local+var", "nt"), "zo::k_sync1<": ("sync1", "nt"),
+            "zo::k_srv_lut<": ("srv", "plain"), f"zo::k_recon<true, {dv}>": ("recon+var", "nt"),
+            "zo::k_copy<true>": ("copy_nt", None), "zo::k_copy<false>": ("copy_plain", None)}
 
 
 def source_hash():
@@ -44,10 +52,12 @@ def source_hash():
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def summarize_pmc(fetch_dir, write_dir, out_path):
+def summarize_pmc(fetch_dir, write_dir, out_path, sync_writes):
     """Turn two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over
     `bench.py --copy-calibration` into per-launch HBM traffic, each counter
-    scaled by what it reads for the calibration copy of COPY_BYTES."""
+    scaled by what it reads for the calibration copy of COPY_BYTES.
+    `sync_writes` names the mode the runs used ("deferred" or "eager")."""
+    keys = kernel_keys(sync_writes)
     def load(d, counter):
         vals = {}
         for root, _, files in os.walk(d):
@@ -58,7 +68,7 @@ def summarize_pmc(fetch_dir, write_dir, out_path):
                     if r["Counter_Name"] != counter:
                         continue
                     name = r["Kernel_Name"].replace("void ", "")
-                    for prefix, (key, _) in KERNEL_KEYS.items():
+                    for prefix, (key, _) in keys.items():
                         if name.startswith(prefix):
                             vals.setdefault(key, []).append(float(r["Counter_Value"]))
         return {k: sum(v) / len(v) for k, v in vals.items()}
@@ -67,13 +77,13 @@ def summarize_pmc(fetch_dir, write_dir, out_path):
                       "write": COPY_BYTES / (1024.0 * write[f"copy_{kind}"])}
                for kind in ("nt", "plain")}
     kernels = {}
-    for prefix, (key, kind) in KERNEL_KEYS.items():
+    for prefix, (key, kind) in keys.items():
         if kind is None or key not in fetch or key not in write:
             continue
         f, w = factors[kind]["fetch"], factors[kind]["write"]
         kernels[key] = {"fetch_kib": fetch[key], "write_kib": write[key], "access": kind,
                         "traffic_bytes": 1024.0 * (fetch[key] * f + write[key] * w)}
-    out = {"source_sha256": source_hash(), "copy_bytes": COPY_BYTES,
+    out = {"source_sha256": source_hash(), "sync_writes": sync_writes, "copy_bytes": COPY_BYTES,
            "copy_kib": {k: {"fetch": fetch[f"copy_{k}"], "write": write[f"copy_{k}"]}
                         for k in ("nt", "plain")},
            "factors": factors, "kernels": kernels}
@@ -82,34 +92,39 @@ def summarize_pmc(fetch_dir, write_dir, out_path):
     print(json.dumps(out, indent=1))
 
 
-def measured_traffic(kernel):
+def measured_traffic(kernel, sync_writes):
     """HBM bytes per launch from the committed counter summary, or None when
-    it is missing or was taken on different kernel source."""
+    it is missing or was taken on different kernel source or another mode."""
     try:
         with open(TRAFFIC_FILE) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
-    if t.get("source_sha256") != source_hash() or kernel not in t.get("kernels", {}):
+    if t.get("source_sha256") != source_hash() or t.get("sync_writes") != sync_writes:
+        return None
+    if kernel not in t.get("kernels", {}):
         return None
     return t["kernels"][kernel]["traffic_bytes"]
 
 
-def algorithmic_bytes(d, nchunks, nwords, W):
+def algorithmic_bytes(d, nchunks, nwords, W, deferred=True):
     """Bytes each kernel must move per launch: every state read once and
-    written once, packed words and per-chunk scales included."""
+    written once, packed words and per-chunk scales included.  With deferred
+    sync writes the local step after a sync reads x from the anchor and does
+    not read u, and the reconstruction writes neither x nor u."""
     pk = 8 * nwords
     sc = 4 * nchunks
     return {
-        # reads g, m, x, v, u, gbar; writes m, x, u, v
-        "local+var": 40 * d,
+        # reads g, m, x, v, u (eager only), gbar; writes m, x, u, v
+        "local+var": (36 if deferred else 40) * d,
         # reads g, m, u, err; writes err, own packed words, own scales
         "sync1": 20 * d + pk + sc,
         # reads W packed buffers + W scale rows + server error;
         # writes server error, server packed words, server scales
         "srv": W * (pk + sc) + 8 * d + pk + sc,
-        # reads server words + scales, v, anchor, gbar; writes m, x, anchor, u, v
-        "recon+var": pk + sc + 32 * d,
+        # reads server words + scales, v, anchor, gbar; writes m, anchor, v,
+        # and x, u (eager only)
+        "recon+var": pk + sc + (24 if deferred else 32) * d,
     }
 
 
@@ -155,13 +170,16 @@ def main():
     ap.add_argument("--workload", default="gpt2-1.5b")
     ap.add_argument("--cpu-sample-chunks", type=int, default=1600)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager-sync-writes", action="store_true",
+                    help="the reconstruction writes x and u at every sync")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run plain and nontemporal copies of a known size (for counters)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
     if args.summarize_pmc:
-        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], TRAFFIC_FILE)
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], TRAFFIC_FILE,
+                      "eager" if args.eager_sync_writes else "deferred")
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the multi-GPU exchange of the method is not "
@@ -215,7 +233,8 @@ def main():
     total_steps = 2 * (args.warmup + args.steps)
     opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=W, chunk=wl.chunk,
                     seg_off=wl.seg_off, tv=list(range(total_steps)),
-                    tu=list(range(1, total_steps, 2)), state=state)
+                    tu=list(range(1, total_steps, 2)), state=state,
+                    defer_sync_writes=not args.eager_sync_writes)
     torch.cuda.synchronize()
     gamma = 1e-4
     names = ("local+var", "sync1", "srv", "recon+var")
@@ -255,7 +274,7 @@ def main():
 
     ms_per_step = wall * 1000.0 / args.steps
     value = 2.0 * d / (ms_per_step / 1000.0)
-    bytes_ = algorithmic_bytes(d, nchunks, nwords, W)
+    bytes_ = algorithmic_bytes(d, nchunks, nwords, W, deferred=not args.eager_sync_writes)
     kernels = {n: {"ms": round(per_kernel[n], 4),
                    "gb_per_launch": round(bytes_[n] / 1e9, 3),
                    "gbs": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0), 1),
@@ -263,7 +282,7 @@ def main():
                for n in names}
     dom = max(names, key=lambda n: per_kernel[n])
     step_bytes = sum(bytes_.values())
-    tb = measured_traffic(dom)
+    tb = measured_traffic(dom, "eager" if args.eager_sync_writes else "deferred")
     traffic_gb = None if tb is None else round(tb / 1e9, 3)
     out = {
         "metric": "0/1 Adam step params/sec and achieved HBM GB/s (% of peak), 1 MI355X",
@@ -282,6 +301,7 @@ def main():
                                f"sync+variance step per bench step",
                    "params": d, "segments": wl.nseg, "world": W, "chunk": wl.chunk,
                    "chunks": nchunks, "server": "single (all chunks)",
+                   "sync_writes": "eager" if args.eager_sync_writes else "deferred",
                    "optimizer_steps_per_bench_step": 2},
         "hbm_gbs_step": round(step_bytes / 1e9 / (ms_per_step / 1000.0), 1),
         "hbm_frac_step": round(step_bytes / 1e9 / (ms_per_step / 1000.0) / HBM_PEAK_GBS, 4),

@@ -77,6 +77,16 @@ typedef struct zo_adam zo_adam;   /* opaque handle */
  *                  chunk range [begin, end) that this GPU serves in the
  *                  server half of Algorithm 2; end < 0 means "to the last
  *                  chunk" (begin = 0, end = -1 is the single server).
+ *   defer_sync_writes
+ *                  0: zo_sync_update writes x, anchor and u = 0 (x and u are
+ *                  always current in their buffers).  Nonzero: it writes only
+ *                  m and the anchor (8 bytes per parameter less); the new
+ *                  model is then held in `anchor` and u is +0 by definition,
+ *                  and the next zo_local_step reads the model from the anchor
+ *                  and does not read u (4 bytes less), writing both back.
+ *                  Until then zo_state_location says where the model is, and
+ *                  zo_materialize writes x and u out.  The arithmetic, and so
+ *                  every value, is the same in both modes.
  */
 typedef struct zo_config {
     float beta1, beta2, eps;
@@ -90,6 +100,7 @@ typedef struct zo_config {
     int32_t ntu;
     const int64_t *tu;
     int64_t srv_chunk_begin, srv_chunk_end;
+    int32_t defer_sync_writes;
 } zo_config;
 
 /*
@@ -186,6 +197,7 @@ int zo_unpack_average(zo_adam *h, int64_t t, const uint64_t *packed, const float
  *   anchor <- x;  u <- 0;  Gamma <- 0  (the next interval starts at t + 1).
  *   srv_packed  device uint64[words], srv_scales device float[nchunks].
  *   gbar        as in zo_local_step: fused variance line when t is in T_v.
+ * With defer_sync_writes, x and u are not written (see zo_config).
  */
 int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const float *srv_scales,
                    const float *gbar);
@@ -197,7 +209,20 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
  */
 int zo_variance_update(zo_adam *h, int64_t t, const float *gbar);
 
+/*
+ * zo_materialize -- with defer_sync_writes, write out what the last
+ * zo_sync_update left implicit: x <- anchor and u <- +0 (one copy and one fill
+ * kernel on the handle's stream, only for what is pending).  Between steps
+ * only (ZO_ESTATE otherwise); changes no value of the optimizer state.  The
+ * next steps run as after an eager zo_sync_update.
+ */
+int zo_materialize(zo_adam *h);
+
 /* ---- queries (host only; never touch the device unless stated) ---------- */
+/* Where the current state is: *x_now = the device buffer that holds x
+ * (st.x, or st.anchor after a deferred zo_sync_update); *u_is_zero = 1 when
+ * u is +0 everywhere and st.u is stale, else 0.  Either pointer may be NULL. */
+int zo_state_location(const zo_adam *h, float **x_now, int32_t *u_is_zero);
 int64_t zo_num_chunks(const zo_adam *h);
 int64_t zo_packed_words(const zo_adam *h);
 /* Server range: first chunk, chunk count, first word, word count, first

@@ -19,7 +19,7 @@ ZO_OK, ZO_EINVAL, ZO_EALIGN, ZO_ESTATE, ZO_EHIP, ZO_ENOMEM = 0, -1, -2, -3, -4, 
 EXPORTS = (
     "zo_adam_init", "zo_adam_destroy", "zo_set_stream", "zo_local_step",
     "zo_compress_pack_ef", "zo_unpack_average", "zo_sync_update", "zo_variance_update",
-    "zo_num_chunks", "zo_packed_words", "zo_server_range", "zo_chunk_table", "zo_gamma_sum",
+    "zo_materialize", "zo_state_location", "zo_num_chunks", "zo_packed_words", "zo_server_range", "zo_chunk_table", "zo_gamma_sum",
     "zo_next_step", "zo_inexact_chunks", "zo_strerror", "zo_last_hip_error",
     "zo_diag_divsqrt", "zo_diag_copy", "zo_config_check", "zo_plan_num_chunks", "zo_plan_chunks",
 )
@@ -40,7 +40,8 @@ class _Config(ctypes.Structure):
                 ("nseg", ctypes.c_int32), ("seg_off", ctypes.POINTER(ctypes.c_int64)),
                 ("ntv", ctypes.c_int32), ("tv", ctypes.POINTER(ctypes.c_int64)),
                 ("ntu", ctypes.c_int32), ("tu", ctypes.POINTER(ctypes.c_int64)),
-                ("srv_chunk_begin", ctypes.c_int64), ("srv_chunk_end", ctypes.c_int64)]
+                ("srv_chunk_begin", ctypes.c_int64), ("srv_chunk_end", ctypes.c_int64),
+                ("defer_sync_writes", ctypes.c_int32)]
 
 
 class _State(ctypes.Structure):
@@ -70,6 +71,8 @@ def lib():
             "zo_unpack_average": ([vp, i64, vp, vp, vp, vp, vp], ci),
             "zo_sync_update": ([vp, i64, vp, vp, vp], ci),
             "zo_variance_update": ([vp, i64, vp], ci),
+            "zo_materialize": ([vp], ci),
+            "zo_state_location": ([vp, ctypes.POINTER(vp), ctypes.POINTER(i32)], ci),
             "zo_num_chunks": ([vp], i64),
             "zo_packed_words": ([vp], i64),
             "zo_server_range": ([vp, pi64, pi64, pi64, pi64, pi64, pi64], ci),
@@ -125,7 +128,7 @@ def _i64_array(values):
 
 
 def make_config(*, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), srv_chunk_begin=0,
-                srv_chunk_end=-1):
+                srv_chunk_end=-1, defer_sync_writes=False):
     """Build a C config; returns (struct, keepalive) -- keep both alive."""
     seg, nseg1 = _i64_array(seg_off)
     tva, ntv = _i64_array(tv)
@@ -135,7 +138,8 @@ def make_config(*, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), srv_c
                   seg_off=ctypes.cast(seg, ctypes.POINTER(ctypes.c_int64)), ntv=ntv,
                   tv=ctypes.cast(tva, ctypes.POINTER(ctypes.c_int64)), ntu=ntu,
                   tu=ctypes.cast(tua, ctypes.POINTER(ctypes.c_int64)),
-                  srv_chunk_begin=int(srv_chunk_begin), srv_chunk_end=int(srv_chunk_end))
+                  srv_chunk_begin=int(srv_chunk_begin), srv_chunk_end=int(srv_chunk_end),
+                  defer_sync_writes=1 if defer_sync_writes else 0)
     return cfg, (seg, tva, tua)
 
 
@@ -204,6 +208,20 @@ def zo_variance_update(h, t, gbar):
     _call(h, "zo_variance_update", int(t), _ptr(gbar))
 
 
+def zo_materialize(h):
+    _call(h, "zo_materialize")
+
+
+def zo_state_location(h):
+    """(device address of the buffer holding x, u_is_zero)."""
+    x = ctypes.c_void_p()
+    uz = ctypes.c_int32()
+    rc = lib().zo_state_location(h, ctypes.byref(x), ctypes.byref(uz))
+    if rc != ZO_OK:
+        raise ZoError(rc, "zo_state_location")
+    return x.value, bool(uz.value)
+
+
 def zo_adam_destroy(h):
     rc = lib().zo_adam_destroy(h)
     if rc != ZO_OK:
@@ -231,10 +249,11 @@ class ZoAdam:
     default)."""
 
     def __init__(self, *, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), state,
-                 srv_chunk_begin=0, srv_chunk_end=-1, stream=None):
+                 srv_chunk_begin=0, srv_chunk_end=-1, defer_sync_writes=False, stream=None):
         self.cfg = dict(beta1=beta1, beta2=beta2, eps=eps, world=world, chunk=chunk,
                         seg_off=list(seg_off), tv=list(tv), tu=list(tu),
-                        srv_chunk_begin=srv_chunk_begin, srv_chunk_end=srv_chunk_end)
+                        srv_chunk_begin=srv_chunk_begin, srv_chunk_end=srv_chunk_end,
+                        defer_sync_writes=defer_sync_writes)
         self.state = state
         self.h = zo_adam_init(self.cfg, state, stream)
 
@@ -269,6 +288,19 @@ class ZoAdam:
 
     def variance_update(self, t, gbar):
         zo_variance_update(self.h, t, gbar)
+
+    def materialize(self):
+        zo_materialize(self.h)
+
+    def current(self, name):
+        """The tensor holding state `name` now (x may live in the anchor after a
+        deferred sync; u then reads as zeros)."""
+        xp, uz = zo_state_location(self.h)
+        if name == "x" and xp == self.state["anchor"].data_ptr():
+            return self.state["anchor"]
+        if name == "u" and uz:
+            return self.state["u"].new_zeros(self.state["u"].shape)
+        return self.state[name]
 
     # queries
     @property

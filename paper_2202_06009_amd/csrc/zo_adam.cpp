@@ -72,6 +72,10 @@ struct zo_adam {
     int phase = PH_IDLE;
     float gamma_sum = 0.0f;
     int srv_algo = zo::SRV_AUTO;
+    // Deferred sync writes: the reconstruction leaves the new model only in
+    // the anchor (x_in_anchor) and u = 0 implicit (u_zero) until the next
+    // local step writes them (or zo_materialize).
+    bool defer = false, x_in_anchor = false, u_zero = false;
     char hip_err[192] = {0};
 
     bool in_tv(int64_t s) const { return std::binary_search(tv.begin(), tv.end(), s); }
@@ -169,6 +173,7 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
     h->stream = stream;
     h->tv.assign(cfg->tv, cfg->tv + cfg->ntv);
     h->tu.assign(cfg->tu, cfg->tu + cfg->ntu);
+    h->defer = cfg->defer_sync_writes != 0;
 
     h->nchunks = zo_plan_num_chunks(cfg->nseg, cfg->seg_off, cfg->chunk);
     std::vector<int64_t> len64;
@@ -284,9 +289,11 @@ int zo_local_step(zo_adam *h, int64_t t, float gamma, const float *g, const floa
     if (gbar && (!tv || tu)) return ZO_EINVAL;
     zo::Scalars s = h->sc;
     s.gamma = gamma;
-    hipError_t e = zo::launch_local(gbar != nullptr, g, h->st.m, h->st.x, h->st.v, h->st.u, gbar,
-                                    h->n, s, h->stream);
+    const float *x_src = h->x_in_anchor ? h->st.anchor : h->st.x;
+    hipError_t e = zo::launch_local(gbar != nullptr, h->u_zero, g, h->st.m, x_src, h->st.x,
+                                    h->st.v, h->st.u, gbar, h->n, s, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
+    h->x_in_anchor = h->u_zero = false;
     h->gamma_sum = h->gamma_sum + gamma;
     if (tu)
         h->phase = PH_LOCAL_SYNC;
@@ -314,8 +321,10 @@ int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const float *g, uint
     }
     zo::Scalars s = h->sc;
     s.gamma = fused ? gamma : 0.0f;
-    hipError_t e = zo::launch_sync1(h->geo, fused, g, h->st.m, h->st.u, h->st.err, h->ch,
-                                    h->nchunks, packed0, scales0, s, h->stream);
+    // (after zo_local_step at this step u has been written, so u_zero is false
+    // on the unfused path)
+    hipError_t e = zo::launch_sync1(h->geo, fused, fused && h->u_zero, g, h->st.m, h->st.u,
+                                    h->st.err, h->ch, h->nchunks, packed0, scales0, s, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     if (fused) h->gamma_sum = h->gamma_sum + gamma;
     h->phase = PH_COMPRESSED;
@@ -351,10 +360,12 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
     if (t != h->t || h->phase != PH_AVERAGED) return ZO_ESTATE;
     const bool tv = h->in_tv(t);
     if (gbar && !tv) return ZO_EINVAL;
-    hipError_t e = zo::launch_recon(h->geo, gbar != nullptr, srv_packed, srv_scales, h->ch,
-                                    h->nchunks, h->st.m, h->st.x, h->st.v, h->st.u, h->st.anchor,
-                                    gbar, h->gamma_sum, h->sc, h->chunk, h->stream);
+    // the deferred kernel reads the anchor, which holds x_{t'} in both cases
+    hipError_t e = zo::launch_recon(h->geo, gbar != nullptr, h->defer, srv_packed, srv_scales,
+                                    h->ch, h->nchunks, h->st.m, h->st.x, h->st.v, h->st.u,
+                                    h->st.anchor, gbar, h->gamma_sum, h->sc, h->chunk, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
+    if (h->defer) h->x_in_anchor = h->u_zero = true;
     h->gamma_sum = 0.0f;
     if (tv && !gbar)
         h->phase = PH_VAR_PENDING;
@@ -372,6 +383,31 @@ int zo_variance_update(zo_adam *h, int64_t t, const float *gbar)
     hipError_t e = zo::launch_var(h->st.v, gbar, h->n, h->sc, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     h->finish_step();
+    return ZO_OK;
+}
+
+int zo_state_location(const zo_adam *h, float **x_now, int32_t *u_is_zero)
+{
+    if (!h) return ZO_EINVAL;
+    if (x_now) *x_now = h->x_in_anchor ? h->st.anchor : h->st.x;
+    if (u_is_zero) *u_is_zero = h->u_zero ? 1 : 0;
+    return ZO_OK;
+}
+
+int zo_materialize(zo_adam *h)
+{
+    if (!h) return ZO_EINVAL;
+    if (h->phase != PH_IDLE) return ZO_ESTATE;
+    if (h->x_in_anchor && h->n > 0) {
+        hipError_t e = zo::launch_copy(h->st.anchor, h->st.x, h->n, true, h->stream);
+        if (e != hipSuccess) return h->hip_fail(e);
+    }
+    h->x_in_anchor = false;
+    if (h->u_zero) {
+        hipError_t e = zo::launch_zero(h->st.u, h->n, h->stream);
+        if (e != hipSuccess) return h->hip_fail(e);
+    }
+    h->u_zero = false;
     return ZO_OK;
 }
 

@@ -32,18 +32,22 @@ Geometry geometry_for(int chunk);
 // Server-average algorithm.
 enum SrvAlgo { SRV_AUTO = 0, SRV_PLAIN = 1 };
 
-hipError_t launch_local(bool var, const float *g, float *m, float *x, float *v, float *u,
-                        const float *gbar, int64_t n, const Scalars &s, hipStream_t st);
+// uz: u is +0 and not read (a deferred reset); x_src may equal x.
+hipError_t launch_local(bool var, bool uz, const float *g, float *m, const float *x_src, float *x,
+                        float *v, float *u, const float *gbar, int64_t n, const Scalars &s,
+                        hipStream_t st);
+hipError_t launch_zero(float *dst, int64_t n, hipStream_t st);
 hipError_t launch_var(float *v, const float *gbar, int64_t n, const Scalars &s, hipStream_t st);
-hipError_t launch_sync1(Geometry geo, bool fused, const float *g, const float *m, const float *u,
-                        float *err, const Chunks &ch, int64_t nchunks, uint64_t *packed,
-                        float *scales, const Scalars &s, hipStream_t st);
+hipError_t launch_sync1(Geometry geo, bool fused, bool uz, const float *g, const float *m,
+                        const float *u, float *err, const Chunks &ch, int64_t nchunks,
+                        uint64_t *packed, float *scales, const Scalars &s, hipStream_t st);
 hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const float *scales, int W,
                       int64_t wstride, int64_t cstride, const Chunks &ch, int64_t c0,
                       int64_t nch, int64_t word0, int64_t elem0, float *srv_err,
                       uint64_t *srv_packed, float *srv_scales, float *avg, uint8_t *flags,
                       int chunk, hipStream_t st);
-hipError_t launch_recon(Geometry geo, bool var, const uint64_t *srv_packed,
+// defer: write m and anchor only (the model stays in the anchor, u = 0 implicit).
+hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const float *gbar,
                         float gsum, const Scalars &s, int chunk, hipStream_t st);

@@ -83,16 +83,21 @@ __device__ __forceinline__ float var_elem(float v, float gb, const Scalars &s)
 // a1 (+a2): local step, one float4 per thread
 // ---------------------------------------------------------------------------
 
-template <bool VAR>
+// The model is read from x_src (x itself, or the anchor when the last
+// synchronisation left the model there) and written to x.  UZ: u is +0
+// everywhere (reset by the last synchronisation and not yet written), so it
+// is not read.
+template <bool VAR, bool UZ>
 __global__ __launch_bounds__(256) void k_local(const float *__restrict__ g, float *__restrict__ m,
-                                               float *__restrict__ x, float *__restrict__ v,
-                                               float *__restrict__ u,
+                                               const float *x_src, float *x,
+                                               float *__restrict__ v, float *__restrict__ u,
                                                const float *__restrict__ gbar, int64_t n4,
                                                Scalars s)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n4) return;
-    f4v gg = ldnt(g, i), mm = ldnt(m, i), xx = ldnt(x, i), vv = ldnt(v, i), uu = ldnt(u, i);
+    f4v gg = ldnt(g, i), mm = ldnt(m, i), xx = ldnt(x_src, i), vv = ldnt(v, i);
+    f4v uu = UZ ? f4v{0.f, 0.f, 0.f, 0.f} : ldnt(u, i);
     f4v gb;
     if (VAR) gb = ldnt(gbar, i);
 #pragma unroll
@@ -266,7 +271,8 @@ __device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, boo
 // buffer lines when g != nullptr)
 // ---------------------------------------------------------------------------
 
-template <int L, int V, bool FUSED>
+// UZ (with FUSED only): u is +0 everywhere and is not read.
+template <int L, int V, bool FUSED, bool UZ>
 __global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
     const float *__restrict__ g, const float *__restrict__ m, const float *__restrict__ u,
     float *__restrict__ err, Chunks ch, int64_t nchunks, uint32_t *__restrict__ packed32,
@@ -286,7 +292,8 @@ __global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
         a[k] = f4v{0.f, 0.f, 0.f, 0.f};
         if (e < len) {
             const int64_t i4 = (e0 + e) >> 2;
-            f4v uu = ldnt(u, i4), dd = ldnt(err, i4);
+            f4v uu = UZ ? f4v{0.f, 0.f, 0.f, 0.f} : ldnt(u, i4);
+            const f4v dd = ldnt(err, i4);
             if (FUSED) {
                 const f4v gg = ldnt(g, i4), mm = ldnt(m, i4);
 #pragma unroll
@@ -672,7 +679,9 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
 // (lb lanes per chunk).
 // ---------------------------------------------------------------------------
 
-template <bool VAR>
+// DEFER: only m and the anchor are written; the new model is the new anchor
+// and u is +0, both left implicit until the next local step writes them.
+template <bool VAR, bool DEFER>
 __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_packed32,
                                                const float *__restrict__ srv_scales, Chunks ch,
                                                int64_t nchunks, int bpc, int lb,
@@ -709,10 +718,20 @@ __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_
         if (VAR) nv[q] = var_elem(vv[q], gb[q], s);
     }
     stnt(m, i4, mm);
-    stnt(x, i4, xx);
     stnt(anchor, i4, xx);
-    stnt(u, i4, f4v{0.f, 0.f, 0.f, 0.f});
+    if (!DEFER) {
+        stnt(x, i4, xx);
+        stnt(u, i4, f4v{0.f, 0.f, 0.f, 0.f});
+    }
     if (VAR) stnt(v, i4, nv);
+}
+
+// dst = +0, one float4 per thread (u after a deferred reset).
+__global__ __launch_bounds__(256) void k_zero(float *__restrict__ dst, int64_t n4)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n4) return;
+    stnt(dst, i, f4v{0.f, 0.f, 0.f, 0.f});
 }
 
 // ---------------------------------------------------------------------------
@@ -805,17 +824,29 @@ static inline unsigned chunk_block() { return L > 256 ? L : 256; }
 template <int L>
 static inline int64_t chunks_per_block() { return L >= 256 ? 1 : 256 / L; }
 
-hipError_t launch_local(bool var, const float *g, float *m, float *x, float *v, float *u,
-                        const float *gbar, int64_t n, const Scalars &s, hipStream_t st)
+hipError_t launch_local(bool var, bool uz, const float *g, float *m, const float *x_src, float *x,
+                        float *v, float *u, const float *gbar, int64_t n, const Scalars &s,
+                        hipStream_t st)
 {
     const int64_t n4 = n / 4;
     if (n4 == 0) return hipSuccess;
-    if (var)
-        hipLaunchKernelGGL(k_local<true>, dim3(grid_for(n4, 256)), dim3(256), 0, st, g, m, x, v,
-                           u, gbar, n4, s);
+    const dim3 grid(grid_for(n4, 256)), block(256);
+    if (var && uz)
+        hipLaunchKernelGGL((k_local<true, true>), grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s);
+    else if (var)
+        hipLaunchKernelGGL((k_local<true, false>), grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s);
+    else if (uz)
+        hipLaunchKernelGGL((k_local<false, true>), grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s);
     else
-        hipLaunchKernelGGL(k_local<false>, dim3(grid_for(n4, 256)), dim3(256), 0, st, g, m, x,
-                           v, u, gbar, n4, s);
+        hipLaunchKernelGGL((k_local<false, false>), grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero(float *dst, int64_t n, hipStream_t st)
+{
+    const int64_t n4 = n / 4;
+    if (n4 == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_zero, dim3(grid_for(n4, 256)), dim3(256), 0, st, dst, n4);
     return hipGetLastError();
 }
 
@@ -827,21 +858,25 @@ hipError_t launch_var(float *v, const float *gbar, int64_t n, const Scalars &s, 
     return hipGetLastError();
 }
 
-hipError_t launch_sync1(Geometry geo, bool fused, const float *g, const float *m, const float *u,
-                        float *err, const Chunks &ch, int64_t nchunks, uint64_t *packed,
-                        float *scales, const Scalars &s, hipStream_t st)
+hipError_t launch_sync1(Geometry geo, bool fused, bool uz, const float *g, const float *m,
+                        const float *u, float *err, const Chunks &ch, int64_t nchunks,
+                        uint64_t *packed, float *scales, const Scalars &s, hipStream_t st)
 {
     if (nchunks == 0) return hipSuccess;
+    if (uz && !fused) return hipErrorInvalidValue;
     return with_geometry(geo, [&](auto Lc, auto Vc) {
         constexpr int L = decltype(Lc)::value, V = decltype(Vc)::value;
         const unsigned grid = grid_for(nchunks, chunks_per_block<L>());
         uint32_t *p32 = reinterpret_cast<uint32_t *>(packed);
-        if (fused)
-            hipLaunchKernelGGL((k_sync1<L, V, true>), dim3(grid), dim3(chunk_block<L>()), 0, st,
-                               g, m, u, err, ch, nchunks, p32, scales, s);
+        if (uz)
+            hipLaunchKernelGGL((k_sync1<L, V, true, true>), dim3(grid), dim3(chunk_block<L>()), 0,
+                               st, g, m, u, err, ch, nchunks, p32, scales, s);
+        else if (fused)
+            hipLaunchKernelGGL((k_sync1<L, V, true, false>), dim3(grid), dim3(chunk_block<L>()),
+                               0, st, g, m, u, err, ch, nchunks, p32, scales, s);
         else
-            hipLaunchKernelGGL((k_sync1<L, V, false>), dim3(grid), dim3(chunk_block<L>()), 0, st,
-                               g, m, u, err, ch, nchunks, p32, scales, s);
+            hipLaunchKernelGGL((k_sync1<L, V, false, false>), dim3(grid), dim3(chunk_block<L>()),
+                               0, st, g, m, u, err, ch, nchunks, p32, scales, s);
         return hipGetLastError();
     });
 }
@@ -928,7 +963,7 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
     }
 }
 
-hipError_t launch_recon(Geometry geo, bool var, const uint64_t *srv_packed,
+hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const float *gbar,
                         float gsum, const Scalars &s, int chunk, hipStream_t st)
@@ -948,12 +983,19 @@ hipError_t launch_recon(Geometry geo, bool var, const uint64_t *srv_packed,
         grid = (nchunks + (256 / lb) - 1) / (256 / lb);
     }
     const uint32_t *p32 = reinterpret_cast<const uint32_t *>(srv_packed);
-    if (var)
-        hipLaunchKernelGGL(k_recon<true>, dim3((unsigned)grid), dim3(256), 0, st, p32, srv_scales,
-                           ch, nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+    const dim3 g3((unsigned)grid), b3(256);
+    if (var && defer)
+        hipLaunchKernelGGL((k_recon<true, true>), g3, b3, 0, st, p32, srv_scales, ch, nchunks, bpc,
+                           lb, m, x, v, u, anchor, gbar, gsum, s);
+    else if (var)
+        hipLaunchKernelGGL((k_recon<true, false>), g3, b3, 0, st, p32, srv_scales, ch, nchunks,
+                           bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+    else if (defer)
+        hipLaunchKernelGGL((k_recon<false, true>), g3, b3, 0, st, p32, srv_scales, ch, nchunks,
+                           bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
     else
-        hipLaunchKernelGGL(k_recon<false>, dim3((unsigned)grid), dim3(256), 0, st, p32,
-                           srv_scales, ch, nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+        hipLaunchKernelGGL((k_recon<false, false>), g3, b3, 0, st, p32, srv_scales, ch, nchunks,
+                           bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
     return hipGetLastError();
 }
 

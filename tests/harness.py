@@ -132,7 +132,7 @@ class OracleRun:
 class GpuRun:
     STATE = ("x", "m", "v", "u", "err", "srv_err", "anchor")
 
-    def __init__(self, wl, device="cuda", fused=True, srv_range=(0, -1)):
+    def __init__(self, wl, device="cuda", fused=True, srv_range=(0, -1), defer=False):
         import torch
         import paper_2202_06009_amd as zo
         self.torch, self.zo, self.wl, self.fused = torch, zo, wl, fused
@@ -154,7 +154,7 @@ class GpuRun:
         self.opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=W,
                              chunk=wl.chunk, seg_off=wl.seg_off, tv=wl.tv, tu=wl.tu,
                              state=self.state, srv_chunk_begin=srv_range[0],
-                             srv_chunk_end=srv_range[1])
+                             srv_chunk_end=srv_range[1], defer_sync_writes=defer)
 
     def fill_inputs(self, t):
         wl = self.wl
@@ -241,7 +241,7 @@ class Comparator:
         w = self.orun.worker
         self.torch.cuda.synchronize()
         for k in GpuRun.STATE:
-            gpu = self.fetch(self.grun.state[k])
+            gpu = self.fetch(self.grun.opt.current(k))
             ref = getattr(w, k)
             if k == "srv_err" and not self.full:
                 pass  # the server range is the whole shard: same indices as elements
@@ -265,9 +265,12 @@ class Comparator:
         return bad
 
 
-def run_parity(wl, steps=None, chunk_ids=None, fused=True, log=None):
-    """Run both sides for `steps` steps; return per-step mismatch dicts."""
-    grun = GpuRun(wl, fused=fused)
+def run_parity(wl, steps=None, chunk_ids=None, fused=True, log=None, defer=False,
+               materialize_at=()):
+    """Run both sides for `steps` steps; return per-step mismatch dicts.
+    defer: deferred sync writes (the logical state is compared);
+    materialize_at: steps after which the deferred writes are forced out."""
+    grun = GpuRun(wl, fused=fused, defer=defer)
     orun = OracleRun(wl, chunk_ids)
     cmp_ = Comparator(grun, orun)
     report = []
@@ -277,6 +280,8 @@ def run_parity(wl, steps=None, chunk_ids=None, fused=True, log=None):
         T = wl.steps if steps is None else steps
         for t in range(T):
             grun.step(t)
+            if t in materialize_at:
+                grun.opt.materialize()
             out = orun.step(t)
             bad = cmp_.check(t, out)
             if log:

@@ -102,3 +102,16 @@ def test_unbuilt_library_raises(monkeypatch, tmp_path):
     monkeypatch.setattr(zo, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         zo.lib()
+
+
+def test_state_calls_reject_null_handle():
+    lib = zo.lib()
+    assert lib.zo_materialize(None) == zo.ZO_EINVAL
+    assert lib.zo_state_location(None, None, None) == zo.ZO_EINVAL
+
+
+def test_config_carries_deferred_writes_flag():
+    cfg, keep = zo.make_config(**_cfg(), defer_sync_writes=True)
+    assert cfg.defer_sync_writes == 1
+    assert zo.zo_config_check(**_cfg(), defer_sync_writes=True) == zo.ZO_OK
+

@@ -72,11 +72,14 @@ def test_device_div_sqrt_are_correctly_rounded(torch_cuda):
 # Tiny workload, whole shard, both readings of its schedule
 # ---------------------------------------------------------------------------
 
+@pytest.mark.parametrize("defer", [False, True], ids=["eager", "defer"])
 @pytest.mark.parametrize("name", ["tiny", "tiny-alt"])
 @pytest.mark.parametrize("fused", [True, False])
-def test_tiny_full_shard(torch_cuda, name, fused):
+def test_tiny_full_shard(torch_cuda, name, fused, defer):
+    """defer: the reconstruction leaves x in the anchor and u implicit; the
+    logical state (x from wherever it lives, u as zeros) must still match."""
     import harness
-    report, inexact = harness.run_parity(C.get(name), fused=fused, log=_log)
+    report, inexact = harness.run_parity(C.get(name), fused=fused, log=_log, defer=defer)
     _assert_clean(report, inexact)
     assert len(report) == C.get(name).steps + 1
 
@@ -122,16 +125,61 @@ def test_small_layouts_full_shard(torch_cuda, segs, chunk, world):
     _assert_clean(report, inexact)
 
 
-def test_single_worker_every_step_syncs(torch_cuda):
+@pytest.mark.parametrize("defer", [False, True], ids=["eager", "defer"])
+def test_single_worker_every_step_syncs(torch_cuda, defer):
     """W = 1 with a sync and a variance update at every step (the setting in
     which the method reduces to Adam) -- exercises the fused variance line in
-    the reconstruction at every step."""
+    the reconstruction at every step; deferred, every compress after the
+    first reads u as the implicit zero and the model stays in the anchor."""
     import harness
     T = 10
     wl = _small("w1-adam", [8192, 4096, 1000], 1024, 1, steps=T, tu=list(range(T)),
                 tv=list(range(T)))
-    report, inexact = harness.run_parity(wl, log=_log)
+    report, inexact = harness.run_parity(wl, log=_log, defer=defer)
     _assert_clean(report, inexact)
+
+
+@pytest.mark.parametrize("segs,chunk,world", [SMALL[0], SMALL[6], SMALL[10]],
+                         ids=["C4-W3", "C256-W16", "C3000-W7"])
+def test_small_layouts_deferred_writes(torch_cuda, segs, chunk, world):
+    """Runs of local steps after deferred syncs, a sync right after a sync
+    (steps 1-2 and 4-5), and the unfused path."""
+    import harness
+    T = 9
+    wl = _small(f"defer-C{chunk}", segs, chunk, world, steps=T, tu=[1, 2, 4, 5, 8],
+                tv=[0, 2, 3, 5])
+    for fused in (True, False):
+        report, inexact = harness.run_parity(wl, log=_log, defer=True, fused=fused)
+        _assert_clean(report, inexact)
+
+
+def test_materialize_after_deferred_sync(torch_cuda):
+    """zo_materialize writes x and u out at any point between steps and the
+    run continues bit for bit."""
+    import harness
+    torch = torch_cuda
+    T = 8
+    wl = _small("materialize", [5000, 1000, 96], 1024, 5, steps=T, tu=[1, 2, 5],
+                tv=[0, 3])
+    report, inexact = harness.run_parity(wl, log=_log, defer=True, materialize_at=(1, 3, 5))
+    _assert_clean(report, inexact)
+    run = harness.GpuRun(wl, defer=True)
+    try:
+        for t in range(3):
+            run.step(t)
+        xp, uz = run.zo.zo_state_location(run.opt.h)
+        assert xp == run.state["anchor"].data_ptr() and uz
+        run.opt.materialize()
+        xp, uz = run.zo.zo_state_location(run.opt.h)
+        assert xp == run.state["x"].data_ptr() and not uz
+        n = wl.n
+        torch.cuda.synchronize()
+        assert torch.equal(run.state["x"][:n].view(torch.int32),
+                           run.state["anchor"][:n].view(torch.int32))
+        assert torch.equal(run.state["u"][:n].view(torch.int32),
+                           torch.zeros(n, dtype=torch.int32, device="cuda"))
+    finally:
+        run.close()
 
 
 def test_local_steps_only(torch_cuda):
@@ -152,6 +200,25 @@ SAMPLED = {
     "bert-large": (600000, 5000),
     "gpt2-1.5b": (500000, 12000),
 }
+
+
+def test_gpt2_sampled_deferred_writes(torch_cuda):
+    """The GPT-2-1.5B shard in the mode and launch shapes the benchmark times
+    (deferred sync writes, fused calls, single server at W = 128)."""
+    import harness
+    import oracle as orc
+    import dataclasses
+    T = 8
+    # the benchmark's alternation: a local step, then a sync step, each with
+    # the variance update
+    wl = dataclasses.replace(C.get("gpt2-1.5b"), name="gpt2-1.5b-alternating", steps=T,
+                             tu=list(range(1, T, 2)), tv=list(range(T)),
+                             gammas=[1e-4] * T)
+    lay = orc.Layout.from_segments(wl.seg_off, wl.chunk)
+    ids = harness.sample_chunks(lay, wl.seg_off, 200000, 24000)
+    _log(f"{wl.name} deferred: {len(ids)} chunks sampled")
+    report, inexact = harness.run_parity(wl, chunk_ids=ids, log=_log, defer=True)
+    _assert_clean(report, inexact)
 
 
 @pytest.mark.timeout(900)
