@@ -128,6 +128,39 @@ def algorithmic_bytes(d, nchunks, nwords, W, deferred=True):
     }
 
 
+def stream_mix_ceilings(zo, torch, state, g, gb, d, deferred):
+    """HBM rate of a plain streaming kernel (zo_diag_stream) with each hot
+    kernel's mix of full-length arrays, on the bench's own buffers (used as
+    scratch after the timed region): the rate such a mix can reach on this
+    GPU.  The server's row-strided packed reads have no such plain mix."""
+    S = state
+    mixes = {
+        "local+var": ([g, gb, S["m"], S["anchor"], S["v"]] + ([] if deferred else [S["u"]]),
+                      [S["x"], S["u"], S["err"], S["srv_err"]] if deferred else
+                      [S["x"], S["err"], S["srv_err"], S["anchor"]]),
+        "sync1": ([g, S["m"], S["u"], S["err"]], [S["x"]]),
+        "recon+var": ([S["v"], S["anchor"], gb],
+                      [S["m"], S["x"], S["u"]] if deferred else
+                      [S["m"], S["x"], S["u"], S["err"]]),
+    }
+    out = {}
+    for name, (src, dst) in mixes.items():
+        best = None
+        for rep in range(4):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            zo.zo_diag_stream(src, dst)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            if rep and (best is None or ms < best):
+                best = ms
+        gbs = (len(src) + len(dst)) * 4.0 * d / 1e9 / (best / 1000.0)
+        out[name] = {"reads": len(src), "writes": len(dst), "gbs": round(gbs, 1),
+                     "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    return out
+
+
 def cpu_baseline(wl, sample_chunks):
     """Time the oracle on the first `sample_chunks` chunks of the shard: one
     local step with variance update and one sync step with variance update,
@@ -271,6 +304,7 @@ def main():
                   / args.steps for i, n in enumerate(names)}
     inexact = opt.inexact_chunks()
     opt.close()
+    mix = stream_mix_ceilings(zo, torch, state, g, gb, d, not args.eager_sync_writes)
 
     ms_per_step = wall * 1000.0 / args.steps
     value = 2.0 * d / (ms_per_step / 1000.0)
@@ -307,6 +341,7 @@ def main():
         "hbm_frac_step": round(step_bytes / 1e9 / (ms_per_step / 1000.0) / HBM_PEAK_GBS, 4),
         "kernels": kernels,
         "inexact_chunks": inexact,
+        "stream_mix_ceiling": mix,
         "roofline": {"bound": "hbm", "kernel": dom,
                      "achieved": kernels[dom]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": kernels[dom]["frac"], "traffic": traffic_gb},

@@ -251,6 +251,15 @@ int zo_diag_divsqrt(const float *a, const float *b, float *q, float *r, int64_t 
  * accesses.  A reference kernel of known size for HBM byte counters. */
 int zo_diag_copy(const float *src, float *dst, int64_t n, int nontemporal, hipStream_t stream);
 
+/* dst[w][i] = (sum over r of src[r][i]) + w for i < n: nsrc in [1, 6] read
+ * streams and ndst in [1, 4] write streams of float[n] (n a multiple of 4,
+ * 16-byte aligned device buffers; src and dst are host arrays of device
+ * pointers; a dst buffer must not be a src buffer), one float4 per thread
+ * with nontemporal accesses like the streaming kernels.  Timing it measures
+ * the HBM rate reachable by a kernel with the same mix of arrays. */
+int zo_diag_stream(const float *const *src, int32_t nsrc, float *const *dst, int32_t ndst,
+                   int64_t n, hipStream_t stream);
+
 /* ---- planning helpers (pure host; usable without a GPU) ----------------- */
 /* Validate a configuration exactly as zo_adam_init does. */
 int zo_config_check(const zo_config *cfg);

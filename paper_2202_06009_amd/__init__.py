@@ -19,9 +19,10 @@ ZO_OK, ZO_EINVAL, ZO_EALIGN, ZO_ESTATE, ZO_EHIP, ZO_ENOMEM = 0, -1, -2, -3, -4, 
 EXPORTS = (
     "zo_adam_init", "zo_adam_destroy", "zo_set_stream", "zo_local_step",
     "zo_compress_pack_ef", "zo_unpack_average", "zo_sync_update", "zo_variance_update",
-    "zo_materialize", "zo_state_location", "zo_num_chunks", "zo_packed_words", "zo_server_range", "zo_chunk_table", "zo_gamma_sum",
-    "zo_next_step", "zo_inexact_chunks", "zo_strerror", "zo_last_hip_error",
-    "zo_diag_divsqrt", "zo_diag_copy", "zo_config_check", "zo_plan_num_chunks", "zo_plan_chunks",
+    "zo_materialize", "zo_state_location", "zo_num_chunks", "zo_packed_words",
+    "zo_server_range", "zo_chunk_table", "zo_gamma_sum", "zo_next_step", "zo_inexact_chunks",
+    "zo_strerror", "zo_last_hip_error", "zo_diag_divsqrt", "zo_diag_copy", "zo_diag_stream",
+    "zo_config_check", "zo_plan_num_chunks", "zo_plan_chunks",
 )
 
 
@@ -84,6 +85,7 @@ def lib():
             "zo_last_hip_error": ([vp], ctypes.c_char_p),
             "zo_diag_divsqrt": ([vp, vp, vp, vp, i64, vp], ci),
             "zo_diag_copy": ([vp, vp, i64, ci, vp], ci),
+            "zo_diag_stream": ([vp, i32, vp, i32, i64, vp], ci),
             "zo_config_check": ([ctypes.POINTER(_Config)], ci),
             "zo_plan_num_chunks": ([i32, vp, i32], i64),
             "zo_plan_chunks": ([i32, vp, i32, vp, vp, vp], i64),
@@ -239,6 +241,19 @@ def zo_diag_copy(src, dst, nontemporal=True, stream=None):
                             _stream(stream))
     if rc != ZO_OK:
         raise ZoError(rc, "zo_diag_copy")
+
+
+def zo_diag_stream(srcs, dsts, stream=None):
+    """dst[w] = sum(srcs) + w over float32 device tensors of one length."""
+    n = srcs[0].numel()
+    for t in list(srcs) + list(dsts):
+        if t.numel() != n:
+            raise ValueError("every stream must have the same length")
+    sa = (ctypes.c_void_p * len(srcs))(*[_ptr(t).value for t in srcs])
+    da = (ctypes.c_void_p * len(dsts))(*[_ptr(t).value for t in dsts])
+    rc = lib().zo_diag_stream(sa, len(srcs), da, len(dsts), n, _stream(stream))
+    if rc != ZO_OK:
+        raise ZoError(rc, "zo_diag_stream")
 
 
 class ZoAdam:

@@ -488,4 +488,24 @@ int zo_diag_copy(const float *src, float *dst, int64_t n, int nontemporal, hipSt
     return e == hipSuccess ? ZO_OK : ZO_EHIP;
 }
 
+int zo_diag_stream(const float *const *src, int32_t nsrc, float *const *dst, int32_t ndst,
+                   int64_t n, hipStream_t stream)
+{
+    if (nsrc < 1 || nsrc > 6 || ndst < 1 || ndst > 4 || !src || !dst) return ZO_EINVAL;
+    if (n < 0 || n % 4) return ZO_EINVAL;
+    zo::StreamPtrs p{};
+    for (int32_t r = 0; r < nsrc; ++r) {
+        if (n > 0 && !src[r]) return ZO_EINVAL;
+        if (!aligned(src[r], 16)) return ZO_EALIGN;
+        p.src[r] = src[r];
+    }
+    for (int32_t w = 0; w < ndst; ++w) {
+        if (n > 0 && !dst[w]) return ZO_EINVAL;
+        if (!aligned(dst[w], 16)) return ZO_EALIGN;
+        p.dst[w] = dst[w];
+    }
+    hipError_t e = zo::launch_stream(nsrc, ndst, p, n, stream);
+    return e == hipSuccess ? ZO_OK : ZO_EHIP;
+}
+
 }  // extern "C"

@@ -52,6 +52,13 @@ hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_
                         float *x, float *v, float *u, float *anchor, const float *gbar,
                         float gsum, const Scalars &s, int chunk, hipStream_t st);
 hipError_t launch_copy(const float *src, float *dst, int64_t n, bool nt, hipStream_t st);
+
+// Streams of the HBM-mix diagnostic: up to 6 read and 4 write arrays.
+struct StreamPtrs {
+    const float *src[6];
+    float *dst[4];
+};
+hipError_t launch_stream(int R, int S, const StreamPtrs &p, int64_t n, hipStream_t st);
 hipError_t launch_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,
                           hipStream_t st);
 

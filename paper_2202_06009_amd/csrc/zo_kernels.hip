@@ -764,6 +764,30 @@ __global__ __launch_bounds__(256) void k_copy(const float *__restrict__ src, flo
         reinterpret_cast<f4v *>(dst)[i] = reinterpret_cast<const f4v *>(src)[i];
 }
 
+// R read streams and S write streams of float4, one float4 per thread per
+// stream, nontemporal: the achievable HBM rate of a streaming kernel's mix of
+// arrays (every write depends on every read, so no load is dead).
+template <int R, int S>
+__global__ __launch_bounds__(256) void k_stream(StreamPtrs p, int64_t n4)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n4) return;
+    f4v acc = f4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const f4v a = ldnt(p.src[r], i);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[q] = acc[q] + a[q];
+    }
+#pragma unroll
+    for (int w = 0; w < S; ++w) {
+        f4v o;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = acc[q] + (float)w;
+        stnt(p.dst[w], i, o);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
@@ -997,6 +1021,35 @@ hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_
         hipLaunchKernelGGL((k_recon<false, false>), g3, b3, 0, st, p32, srv_scales, ch, nchunks,
                            bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
     return hipGetLastError();
+}
+
+template <int R>
+static hipError_t stream_r(int S, const StreamPtrs &p, int64_t n4, hipStream_t st)
+{
+    const dim3 grid(grid_for(n4, 256)), block(256);
+    switch (S) {
+    case 1: hipLaunchKernelGGL((k_stream<R, 1>), grid, block, 0, st, p, n4); break;
+    case 2: hipLaunchKernelGGL((k_stream<R, 2>), grid, block, 0, st, p, n4); break;
+    case 3: hipLaunchKernelGGL((k_stream<R, 3>), grid, block, 0, st, p, n4); break;
+    case 4: hipLaunchKernelGGL((k_stream<R, 4>), grid, block, 0, st, p, n4); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_stream(int R, int S, const StreamPtrs &p, int64_t n, hipStream_t st)
+{
+    const int64_t n4 = n / 4;
+    if (n4 == 0) return hipSuccess;
+    switch (R) {
+    case 1: return stream_r<1>(S, p, n4, st);
+    case 2: return stream_r<2>(S, p, n4, st);
+    case 3: return stream_r<3>(S, p, n4, st);
+    case 4: return stream_r<4>(S, p, n4, st);
+    case 5: return stream_r<5>(S, p, n4, st);
+    case 6: return stream_r<6>(S, p, n4, st);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_copy(const float *src, float *dst, int64_t n, bool nt, hipStream_t st)

@@ -1,6 +1,7 @@
 """CPU checks of the C-ABI library: it loads, exports every function the
 headers declare, and its host-only logic (validation, chunk planning) works
 without a GPU.  No kernel is launched here."""
+import ctypes
 import glob
 import os
 import re
@@ -115,3 +116,13 @@ def test_config_carries_deferred_writes_flag():
     assert cfg.defer_sync_writes == 1
     assert zo.zo_config_check(**_cfg(), defer_sync_writes=True) == zo.ZO_OK
 
+
+
+def test_diag_stream_validates_before_touching_the_device():
+    lib = zo.lib()
+    assert lib.zo_diag_stream(None, 1, None, 1, 16, None) == zo.ZO_EINVAL
+    arr = (ctypes.c_void_p * 7)()
+    assert lib.zo_diag_stream(arr, 7, arr, 1, 16, None) == zo.ZO_EINVAL   # too many reads
+    assert lib.zo_diag_stream(arr, 1, arr, 5, 16, None) == zo.ZO_EINVAL   # too many writes
+    assert lib.zo_diag_stream(arr, 1, arr, 1, 6, None) == zo.ZO_EINVAL    # n not a multiple of 4
+    assert lib.zo_diag_stream(arr, 1, arr, 1, 16, None) == zo.ZO_EINVAL   # null buffers

@@ -204,3 +204,22 @@ def test_runs_are_deterministic(torch_cuda):
     finally:
         a.close()
         b.close()
+
+
+def test_diag_stream_mix(torch_cuda):
+    """The stream-mix diagnostic computes dst[w] = (sum of sources in order) + w."""
+    import paper_2202_06009_amd as zo
+    torch = torch_cuda
+    n = (1 << 20) + 12
+    r = np.random.default_rng(7)
+    host = [r.standard_normal(n).astype(np.float32) for _ in range(5)]
+    src = [torch.from_numpy(h).cuda() for h in host]
+    dst = [torch.empty(n, dtype=torch.float32, device="cuda") for _ in range(4)]
+    zo.zo_diag_stream(src, dst)
+    torch.cuda.synchronize()
+    acc = np.zeros(n, np.float32)
+    for h in host:
+        acc = (acc + h).astype(np.float32)
+    for w in range(4):
+        ref = (acc + np.float32(w)).astype(np.float32)
+        assert np.array_equal(dst[w].cpu().numpy(), ref)
