@@ -6,7 +6,8 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 
 The arithmetic lives in ``zo_oracle.c`` (plain single-threaded C, binary32
 with every rounding pinned); this module only marshals numpy arrays and
-orders the calls the way Algorithm 1 of the paper orders its lines:
+orders the calls the way Algorithm 1 of the paper orders its lines
+(``Worker``; ``FVWorker`` does the same for Algorithm 4):
 momentum / model / buffer, then the sync block (Algorithm 2 worker half, the
 server half, momentum approximation and model reconstruction), then the
 variance block.  ``brute_adam`` holds an independent binary64 Adam (the
@@ -77,6 +78,9 @@ def _load():
     lib.zr_sync_dense.restype = None
     lib.zr_variance.argtypes = [ctypes.POINTER(_Params), ctypes.POINTER(_State), i64, _f32p]
     lib.zr_variance.restype = None
+    lib.zr_fv_step.argtypes = [ctypes.POINTER(_Params), _f32p, _f32p, _f32p, i64, f32, _f32p,
+                               i32]
+    lib.zr_fv_step.restype = None
     return lib
 
 
@@ -320,3 +324,46 @@ class Worker:
         if var:
             self.variance(g if gbar is None else gbar)
         return out
+
+
+class FVWorker:
+    """One worker's state under Algorithm 4 (the frozen-variance framework;
+    1-bit Adam when T_v is a prefix of the steps): model x, momentum m,
+    variance v, worker error delta and server error of Algorithm 2, which
+    compresses the gradients at every step outside T_v."""
+
+    def __init__(self, layout, x0, beta1=0.9, beta2=0.999, eps=1e-8):
+        self.layout = layout
+        n = layout.n
+        self.params = _Params()
+        lib().zr_params_init(ctypes.byref(self.params), beta1, beta2, eps, 0)
+        self.x = np.array(x0, dtype=np.float32, copy=True)
+        self.m = np.zeros(n, np.float32)
+        self.v = np.zeros(n, np.float32)
+        self.err = np.zeros(n, np.float32)
+        self.srv_err = np.zeros(n, np.float32)
+
+    def apply(self, gamma, gbar, update_v):
+        lib().zr_fv_step(ctypes.byref(self.params), self.x, self.m, self.v, self.layout.n,
+                         float(gamma), np.ascontiguousarray(gbar, np.float32),
+                         1 if update_v else 0)
+
+    def step(self, gamma, g, full, gbar=None, peer_words=None, peer_scales=None):
+        """One step for worker 0.  full (t in T_v): gbar is the full-precision
+        average.  Otherwise g is compressed with the worker error, averaged
+        with the peers' packed buffers by the server (with the server error)
+        and the server's compressed average is the step's gradient.
+        Returns the own and server packed outputs of a compressed step."""
+        if full:
+            self.apply(gamma, g if gbar is None else gbar, True)
+            return {}
+        own_w, own_s = ef_compress(self.layout, g, self.err)
+        if peer_words is not None and len(peer_words):
+            words_w = np.concatenate([own_w[None, :], peer_words], axis=0)
+            scales_w = np.concatenate([own_s[None, :], peer_scales], axis=0)
+        else:
+            words_w, scales_w = own_w[None, :], own_s[None, :]
+        sw, ss, _ = server(self.layout, words_w, scales_w, self.srv_err)
+        self.apply(gamma, decompress(self.layout, sw, ss), False)
+        return dict(own_words=own_w, own_scales=own_s, srv_words=sw, srv_scales=ss)
+

@@ -7,6 +7,9 @@
  *
  * What it computes (Lu, Li, Zhang, De Sa, He, "Maximizing Communication
  * Efficiency for Large-scale Training via 0/1 Adam", arXiv 2202.06009):
+ *   - Algorithm 4 (the frozen-variance framework with compressed gradients,
+ *     of which 1-bit Adam is the case T_v = a prefix of the steps), one step
+ *     given the averaged gradient, see zr_fv_step;
  *   - Algorithm 1 (0/1 Adam) for one worker, step by step, in the paper's
  *     order: momentum, model, buffer; then the sync block (1bit-AllReduce of
  *     the buffer, momentum approximation, model from the anchor, reset); then
@@ -355,3 +358,30 @@ void zr_variance(const zr_params *p, zr_state *st, int64_t n, const float *gbar)
     for (int64_t j = 0; j < n; ++j)
         st->v[j] = p->beta2 * st->v[j] + p->c2 * (gbar[j] * gbar[j]);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Algorithm 4: 1-bit communication with a frozen variance (no local steps). */
+/* ------------------------------------------------------------------------ */
+
+/* One step of Algorithm 4 given the averaged gradient gbar: the
+ * full-precision average at t in T_v (update_v = 1), else the compressed
+ * average of Algorithm 2 applied to the gradients (update_v = 0).  The
+ * listing's lines in its order:
+ *   v_{t+1} = beta2 v_t + (1 - beta2) gbar^2   (t in T_v;  else v_{t+1} = v_t)
+ *   m_{t+1} = beta1 m_t + (1 - beta1) gbar
+ *   x_{t+1} = x_t - gamma_t m_t / sqrt(v_t + eps)
+ * The model line uses m_t and v_t as printed, as Equation 2 does: nothing
+ * here degenerates, so the listing is taken literally. */
+void zr_fv_step(const zr_params *p, float *x, float *m, float *v, int64_t n, float gamma,
+                const float *gbar, int32_t update_v)
+{
+    for (int64_t j = 0; j < n; ++j) {
+        float v_old = v[j], m_old = m[j];
+        if (update_v) v[j] = p->beta2 * v_old + p->c2 * (gbar[j] * gbar[j]);
+        m[j] = p->beta1 * m_old + p->c1 * gbar[j];
+        float step = gamma * m_old;
+        float den = sqrtf(v_old + p->eps);
+        x[j] = x[j] - step / den;
+    }
+}
+
