@@ -40,11 +40,15 @@ COPY_BYTES = 4 << 30          # size of the calibration copies
 # uses one kind of access (nontemporal or plain), calibrated by the matching copy.
 # The second template argument of k_local / k_recon is the deferred variant
 # (the very first local step of a run has no sync before it and is skipped).
-def kernel_keys(sync_writes):
-    dv = "true" if sync_writes == "deferred" else "false"
+def kernel_keys(mode):
+    copies = {"zo::k_copy<true>": ("copy_nt", None), "zo::k_copy<false>": ("copy_plain", None)}
+    if mode == "frozen-variance":
+        return {"zo::k_fv_full": ("fv_full", "nt"), "zo::k_sync1<": ("sync1", "nt"),
+                "zo::k_srv_lut<": ("srv", "plain"), "zo::k_fv_apply": ("fv_apply", "nt")} | copies
+    dv = "true" if mode == "deferred" else "false"
     return {f"zo::k_local<true, {dv}>": ("local+var", "nt"), "zo::k_sync1<": ("sync1", "nt"),
-            "zo::k_srv_lut<": ("srv", "plain"), f"zo::k_recon<true, {dv}>": ("recon+var", "nt"),
-            "zo::k_copy<true>": ("copy_nt", None), "zo::k_copy<false>": ("copy_plain", None)}
+            "zo::k_srv_lut<": ("srv", "plain"), f"zo::k_recon<true, {dv}>": ("recon+var", "nt")
+            } | copies
 
 
 def source_hash():
@@ -52,12 +56,13 @@ def source_hash():
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def summarize_pmc(fetch_dir, write_dir, out_path, sync_writes):
+def summarize_pmc(fetch_dir, write_dir, out_path, mode):
     """Turn two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over
     `bench.py --copy-calibration` into per-launch HBM traffic, each counter
     scaled by what it reads for the calibration copy of COPY_BYTES.
-    `sync_writes` names the mode the runs used ("deferred" or "eager")."""
-    keys = kernel_keys(sync_writes)
+    `mode` names what the runs timed: "deferred" or "eager" sync writes of
+    Algorithm 1, or "frozen-variance" (Algorithm 4)."""
+    keys = kernel_keys(mode)
     def load(d, counter):
         vals = {}
         for root, _, files in os.walk(d):
@@ -83,7 +88,7 @@ def summarize_pmc(fetch_dir, write_dir, out_path, sync_writes):
         f, w = factors[kind]["fetch"], factors[kind]["write"]
         kernels[key] = {"fetch_kib": fetch[key], "write_kib": write[key], "access": kind,
                         "traffic_bytes": 1024.0 * (fetch[key] * f + write[key] * w)}
-    out = {"source_sha256": source_hash(), "sync_writes": sync_writes, "copy_bytes": COPY_BYTES,
+    out = {"source_sha256": source_hash(), "mode": mode, "copy_bytes": COPY_BYTES,
            "copy_kib": {k: {"fetch": fetch[f"copy_{k}"], "write": write[f"copy_{k}"]}
                         for k in ("nt", "plain")},
            "factors": factors, "kernels": kernels}
@@ -92,7 +97,7 @@ def summarize_pmc(fetch_dir, write_dir, out_path, sync_writes):
     print(json.dumps(out, indent=1))
 
 
-def measured_traffic(kernel, sync_writes):
+def measured_traffic(kernel, mode):
     """HBM bytes per launch from the committed counter summary, or None when
     it is missing or was taken on different kernel source or another mode."""
     try:
@@ -100,11 +105,26 @@ def measured_traffic(kernel, sync_writes):
             t = json.load(fh)
     except (OSError, ValueError):
         return None
-    if t.get("source_sha256") != source_hash() or t.get("sync_writes") != sync_writes:
+    if t.get("source_sha256") != source_hash() or t.get("mode") != mode:
         return None
     if kernel not in t.get("kernels", {}):
         return None
     return t["kernels"][kernel]["traffic_bytes"]
+
+
+def algorithmic_bytes_fv(d, nchunks, nwords, W):
+    """Algorithm 4: bytes each kernel must move per launch."""
+    pk = 8 * nwords
+    sc = 4 * nchunks
+    return {
+        # reads gbar, x, m, v; writes x, m, v
+        "fv_full": 28 * d,
+        # reads g, err; writes err, own packed words, own scales
+        "sync1": 12 * d + pk + sc,
+        "srv": W * (pk + sc) + 8 * d + pk + sc,
+        # reads server words + scales, x, m, v; writes x, m
+        "fv_apply": pk + sc + 20 * d,
+    }
 
 
 def algorithmic_bytes(d, nchunks, nwords, W, deferred=True):
@@ -128,13 +148,18 @@ def algorithmic_bytes(d, nchunks, nwords, W, deferred=True):
     }
 
 
-def stream_mix_ceilings(zo, torch, state, g, gb, d, deferred):
+def stream_mix_ceilings(zo, torch, state, g, gb, d, mode):
     """HBM rate of a plain streaming kernel (zo_diag_stream) with each hot
     kernel's mix of full-length arrays, on the bench's own buffers (used as
     scratch after the timed region): the rate such a mix can reach on this
     GPU.  The server's row-strided packed reads have no such plain mix."""
     S = state
+    deferred = mode == "deferred"
     mixes = {
+        "fv_full": ([gb, S["x"], S["m"], S["v"]], [S["u"], S["err"], S["srv_err"]]),
+        "sync1": ([g, S["err"]], [S["x"]]),
+        "fv_apply": ([S["x"], S["m"], S["v"]], [S["u"], S["anchor"]]),
+    } if mode == "frozen-variance" else {
         "local+var": ([g, gb, S["m"], S["anchor"], S["v"]] + ([] if deferred else [S["u"]]),
                       [S["x"], S["u"], S["err"], S["srv_err"]] if deferred else
                       [S["x"], S["err"], S["srv_err"], S["anchor"]]),
@@ -161,10 +186,11 @@ def stream_mix_ceilings(zo, torch, state, g, gb, d, deferred):
     return out
 
 
-def cpu_baseline(wl, sample_chunks):
+def cpu_baseline(wl, sample_chunks, fv=False):
     """Time the oracle on the first `sample_chunks` chunks of the shard: one
-    local step with variance update and one sync step with variance update,
-    W = 128 (input generation excluded)."""
+    local step with variance update and one sync step with variance update
+    (Algorithm 4: one full-precision and one compressed step), W = 128
+    (input generation excluded)."""
     import numpy as np
     import oracle as orc
     import synth
@@ -180,19 +206,27 @@ def cpu_baseline(wl, sample_chunks):
     gb = synth.normal_host(n, 0, synth.key(0, C.STREAM_GBAR, 0), ks, wl.outlier_per_mille,
                            wl.outlier_factor)
     W = wl.world
-    base = np.float32(2 * 1e-4 * 0.18 * wl.sigma_g)
+    base = np.float32(0.8 * wl.sigma_g if fv else 2 * 1e-4 * 0.18 * wl.sigma_g)
     pw = np.stack([synth.bits_host(lay.nwords, 0, synth.key(w, C.STREAM_BITS, 1))
                    for w in range(1, W)])
     ps = np.stack([synth.scales_host(nch, 0, synth.key(w, C.STREAM_SCALES, 1), base)
                    for w in range(1, W)])
-    worker = orc.Worker(lay, x0, wl.beta1, wl.beta2, wl.eps)
-    t0 = time.perf_counter()
-    worker.step(np.float32(1e-4), g, False, True, gbar=gb)
-    worker.step(np.float32(1e-4), g, True, True, gbar=gb, peer_words=pw, peer_scales=ps)
+    if fv:
+        worker = orc.FVWorker(lay, x0, wl.beta1, wl.beta2, wl.eps)
+        t0 = time.perf_counter()
+        worker.step(np.float32(1e-4), g, True, gbar=gb)
+        worker.step(np.float32(1e-4), g, False, peer_words=pw, peer_scales=ps)
+        what = "one full-precision and one compressed step of Algorithm 4"
+    else:
+        worker = orc.Worker(lay, x0, wl.beta1, wl.beta2, wl.eps)
+        t0 = time.perf_counter()
+        worker.step(np.float32(1e-4), g, False, True, gbar=gb)
+        worker.step(np.float32(1e-4), g, True, True, gbar=gb, peer_words=pw, peer_scales=ps)
+        what = "one local+variance step and one sync+variance step"
     dt = time.perf_counter() - t0
     return {"value": 2 * n / dt, "unit": "params/s", "cores": 1, "kind": "oracle",
-            "sample": f"first {nch} chunks ({n} params) of the same shard, W={W}: one "
-                      f"local+variance step and one sync+variance step, {dt:.2f} s"}
+            "sample": f"first {nch} chunks ({n} params) of the same shard, W={W}: {what}, "
+                      f"{dt:.2f} s"}
 
 
 def main():
@@ -205,14 +239,18 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager-sync-writes", action="store_true",
                     help="the reconstruction writes x and u at every sync")
+    ap.add_argument("--algorithm", choices=("zero-one", "frozen-variance"), default="zero-one",
+                    help="frozen-variance: Algorithm 4 (1-bit Adam's compression stage), one "
+                         "full-precision and one compressed step per bench step")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run plain and nontemporal copies of a known size (for counters)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
+    fv = args.algorithm == "frozen-variance"
+    mode = "frozen-variance" if fv else ("eager" if args.eager_sync_writes else "deferred")
     if args.summarize_pmc:
-        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], TRAFFIC_FILE,
-                      "eager" if args.eager_sync_writes else "deferred")
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], TRAFFIC_FILE, mode)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the multi-GPU exchange of the method is not "
@@ -258,27 +296,36 @@ def main():
                      wl.outlier_factor)
     synth.normal_dev(gb, 0, synth.key(0, C.STREAM_GBAR, 0), ks, wl.outlier_per_mille,
                      wl.outlier_factor)
-    base = 2 * 1e-4 * 0.18 * wl.sigma_g
+    # peers compress u (two steps of gamma m) under Algorithm 1, g under Algorithm 4
+    base = 0.8 * wl.sigma_g if fv else 2 * 1e-4 * 0.18 * wl.sigma_g
     for w in range(1, W):
         synth.bits_dev(packed[w], 0, synth.key(w, C.STREAM_BITS, 1))
         synth.scales_dev(scales[w], 0, synth.key(w, C.STREAM_SCALES, 1), base)
 
     total_steps = 2 * (args.warmup + args.steps)
-    opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=W, chunk=wl.chunk,
-                    seg_off=wl.seg_off, tv=list(range(total_steps)),
-                    tu=list(range(1, total_steps, 2)), state=state,
-                    defer_sync_writes=not args.eager_sync_writes)
+    if fv:
+        opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=W, chunk=wl.chunk,
+                        seg_off=wl.seg_off, tv=list(range(0, total_steps, 2)), tu=[],
+                        state=state, algorithm="frozen-variance")
+        names = ("fv_full", "sync1", "srv", "fv_apply")
+    else:
+        opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=W, chunk=wl.chunk,
+                        seg_off=wl.seg_off, tv=list(range(total_steps)),
+                        tu=list(range(1, total_steps, 2)), state=state,
+                        defer_sync_writes=not args.eager_sync_writes)
+        names = ("local+var", "sync1", "srv", "recon+var")
     torch.cuda.synchronize()
     gamma = 1e-4
-    names = ("local+var", "sync1", "srv", "recon+var")
 
     def bench_step(k, ev=None):
         t = 2 * k
+        first = (lambda: opt.fullprec_step(t, gamma, gb)) if fv else \
+            (lambda: opt.local_step(t, gamma, g, gb))
         calls = (
-            lambda: opt.local_step(t, gamma, g, gb),
+            first,
             lambda: opt.compress_pack_ef(t + 1, gamma, g, packed[0], scales[0]),
             lambda: opt.unpack_average(t + 1, packed, scales, srv_packed, srv_scales),
-            lambda: opt.sync_update(t + 1, srv_packed, srv_scales, gb),
+            lambda: opt.sync_update(t + 1, srv_packed, srv_scales, None if fv else gb),
         )
         for i, call in enumerate(calls):
             if ev is not None:
@@ -304,11 +351,12 @@ def main():
                   / args.steps for i, n in enumerate(names)}
     inexact = opt.inexact_chunks()
     opt.close()
-    mix = stream_mix_ceilings(zo, torch, state, g, gb, d, not args.eager_sync_writes)
+    mix = stream_mix_ceilings(zo, torch, state, g, gb, d, mode)
 
     ms_per_step = wall * 1000.0 / args.steps
     value = 2.0 * d / (ms_per_step / 1000.0)
-    bytes_ = algorithmic_bytes(d, nchunks, nwords, W, deferred=not args.eager_sync_writes)
+    bytes_ = algorithmic_bytes_fv(d, nchunks, nwords, W) if fv else \
+        algorithmic_bytes(d, nchunks, nwords, W, deferred=not args.eager_sync_writes)
     kernels = {n: {"ms": round(per_kernel[n], 4),
                    "gb_per_launch": round(bytes_[n] / 1e9, 3),
                    "gbs": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0), 1),
@@ -316,7 +364,7 @@ def main():
                for n in names}
     dom = max(names, key=lambda n: per_kernel[n])
     step_bytes = sum(bytes_.values())
-    tb = measured_traffic(dom, "eager" if args.eager_sync_writes else "deferred")
+    tb = measured_traffic(dom, mode)
     traffic_gb = None if tb is None else round(tb / 1e9, 3)
     out = {
         "metric": "0/1 Adam step params/sec and achieved HBM GB/s (% of peak), 1 MI355X",
@@ -331,11 +379,15 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{wl.name} flat shard, one local+variance step and one "
-                               f"sync+variance step per bench step",
+        "config": {"workload": f"{wl.name} flat shard, " + (
+                       "Algorithm 4: one full-precision and one compressed step per bench step"
+                       if fv else "one local+variance step and one sync+variance step per "
+                                  "bench step"),
+                   "algorithm": args.algorithm,
                    "params": d, "segments": wl.nseg, "world": W, "chunk": wl.chunk,
                    "chunks": nchunks, "server": "single (all chunks)",
-                   "sync_writes": "eager" if args.eager_sync_writes else "deferred",
+                   "sync_writes": None if fv else ("eager" if args.eager_sync_writes
+                                                   else "deferred"),
                    "optimizer_steps_per_bench_step": 2},
         "hbm_gbs_step": round(step_bytes / 1e9 / (ms_per_step / 1000.0), 1),
         "hbm_frac_step": round(step_bytes / 1e9 / (ms_per_step / 1000.0) / HBM_PEAK_GBS, 4),
@@ -348,7 +400,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_chunks)
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_chunks, fv)
     print(json.dumps(out), flush=True)
 
 

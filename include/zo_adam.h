@@ -59,6 +59,14 @@ enum {
     ZO_ENOMEM = -5    /* host or device allocation failed in zo_adam_init */
 };
 
+/* Algorithms (zo_config.algorithm). */
+enum {
+    ZO_ALG_ZERO_ONE_ADAM = 0,     /* Algorithm 1 with Algorithm 2 (0/1 Adam) */
+    ZO_ALG_FROZEN_VARIANCE = 1    /* Algorithm 4 with Algorithm 2: 1-bit compressed
+                                     gradients, variance updated only in T_v, no local
+                                     steps; 1-bit Adam is T_v = {0, ..., T0 - 1} */
+};
+
 typedef struct zo_adam zo_adam;   /* opaque handle */
 
 /*
@@ -87,6 +95,12 @@ typedef struct zo_adam zo_adam;   /* opaque handle */
  *                  Until then zo_state_location says where the model is, and
  *                  zo_materialize writes x and u out.  The arithmetic, and so
  *                  every value, is the same in both modes.
+ *   algorithm      ZO_ALG_ZERO_ONE_ADAM (default 0) or ZO_ALG_FROZEN_VARIANCE.
+ *                  The latter requires ntu = 0 and defer_sync_writes = 0; its
+ *                  steps are zo_fullprec_step at t in T_v and, at every other
+ *                  t, zo_compress_pack_ef (with the gradient), zo_unpack_average
+ *                  and zo_sync_update (gbar = NULL).  st.u and st.anchor are
+ *                  unused and may be NULL.
  */
 typedef struct zo_config {
     float beta1, beta2, eps;
@@ -101,6 +115,7 @@ typedef struct zo_config {
     const int64_t *tu;
     int64_t srv_chunk_begin, srv_chunk_end;
     int32_t defer_sync_writes;
+    int32_t algorithm;
 } zo_config;
 
 /*
@@ -161,6 +176,9 @@ int zo_local_step(zo_adam *h, int64_t t, float gamma, const float *g, const floa
  * with m' = beta1 m + (1 - beta1) g, and Gamma += gamma; x, m and u are not
  * written (the reconstruction supersedes them).  With g == NULL the call must
  * follow zo_local_step(t) and u already holds u_{t+1/2} (gamma is ignored).
+ * ZO_ALG_FROZEN_VARIANCE, t not in T_v: a = g + err (the compressed
+ * AllReduce of the gradient in Algorithm 4); g is required and gamma = gamma_t
+ * is kept for zo_sync_update.
  *   packed0  device uint64[words]: this worker's packed signs (slot 0).
  *   scales0  device float[nchunks]: this worker's scales (slot 0).
  */
@@ -198,9 +216,24 @@ int zo_unpack_average(zo_adam *h, int64_t t, const uint64_t *packed, const float
  *   srv_packed  device uint64[words], srv_scales device float[nchunks].
  *   gbar        as in zo_local_step: fused variance line when t is in T_v.
  * With defer_sync_writes, x and u are not written (see zo_config).
+ * ZO_ALG_FROZEN_VARIANCE: gbar_t = sigma s is the step's gradient in
+ * Algorithm 4's momentum and model lines, v is kept (t is not in T_v):
+ *   m <- beta1 m + (1 - beta1) gbar_t;  x <- x - gamma_t m_t / sqrt(v_t + eps)
+ * with the momentum m_t and variance v_t from before the step, as the listing
+ * writes them; gbar must be NULL.
  */
 int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const float *srv_scales,
                    const float *gbar);
+
+/*
+ * zo_fullprec_step -- ZO_ALG_FROZEN_VARIANCE, t in T_v: one step of
+ * Algorithm 4 with the full-precision AllReduce output gbar (device float[n]):
+ *   v <- beta2 v + (1 - beta2) gbar^2;  m <- beta1 m + (1 - beta1) gbar;
+ *   x <- x - gamma m_t / sqrt(v_t + eps)   (m_t, v_t from before the step).
+ * ZO_EINVAL on a ZO_ALG_ZERO_ONE_ADAM handle; ZO_ESTATE if t is not the next
+ * step or not in T_v.
+ */
+int zo_fullprec_step(zo_adam *h, int64_t t, float gamma, const float *gbar);
 
 /*
  * zo_variance_update -- the variance line of Algorithm 1 for t in T_v when it

@@ -14,12 +14,14 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libzoadam.so")
 
 ZO_OK, ZO_EINVAL, ZO_EALIGN, ZO_ESTATE, ZO_EHIP, ZO_ENOMEM = 0, -1, -2, -3, -4, -5
+ZO_ALG_ZERO_ONE_ADAM, ZO_ALG_FROZEN_VARIANCE = 0, 1
+ALGORITHMS = {"zero-one": ZO_ALG_ZERO_ONE_ADAM, "frozen-variance": ZO_ALG_FROZEN_VARIANCE}
 
 # Every function the header declares (checked by the CPU export test).
 EXPORTS = (
     "zo_adam_init", "zo_adam_destroy", "zo_set_stream", "zo_local_step",
     "zo_compress_pack_ef", "zo_unpack_average", "zo_sync_update", "zo_variance_update",
-    "zo_materialize", "zo_state_location", "zo_num_chunks", "zo_packed_words",
+    "zo_fullprec_step", "zo_materialize", "zo_state_location", "zo_num_chunks", "zo_packed_words",
     "zo_server_range", "zo_chunk_table", "zo_gamma_sum", "zo_next_step", "zo_inexact_chunks",
     "zo_strerror", "zo_last_hip_error", "zo_diag_divsqrt", "zo_diag_copy", "zo_diag_stream",
     "zo_config_check", "zo_plan_num_chunks", "zo_plan_chunks",
@@ -42,7 +44,7 @@ class _Config(ctypes.Structure):
                 ("ntv", ctypes.c_int32), ("tv", ctypes.POINTER(ctypes.c_int64)),
                 ("ntu", ctypes.c_int32), ("tu", ctypes.POINTER(ctypes.c_int64)),
                 ("srv_chunk_begin", ctypes.c_int64), ("srv_chunk_end", ctypes.c_int64),
-                ("defer_sync_writes", ctypes.c_int32)]
+                ("defer_sync_writes", ctypes.c_int32), ("algorithm", ctypes.c_int32)]
 
 
 class _State(ctypes.Structure):
@@ -73,6 +75,7 @@ def lib():
             "zo_sync_update": ([vp, i64, vp, vp, vp], ci),
             "zo_variance_update": ([vp, i64, vp], ci),
             "zo_materialize": ([vp], ci),
+            "zo_fullprec_step": ([vp, i64, f32, vp], ci),
             "zo_state_location": ([vp, ctypes.POINTER(vp), ctypes.POINTER(i32)], ci),
             "zo_num_chunks": ([vp], i64),
             "zo_packed_words": ([vp], i64),
@@ -130,7 +133,7 @@ def _i64_array(values):
 
 
 def make_config(*, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), srv_chunk_begin=0,
-                srv_chunk_end=-1, defer_sync_writes=False):
+                srv_chunk_end=-1, defer_sync_writes=False, algorithm="zero-one"):
     """Build a C config; returns (struct, keepalive) -- keep both alive."""
     seg, nseg1 = _i64_array(seg_off)
     tva, ntv = _i64_array(tv)
@@ -141,7 +144,8 @@ def make_config(*, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), srv_c
                   tv=ctypes.cast(tva, ctypes.POINTER(ctypes.c_int64)), ntu=ntu,
                   tu=ctypes.cast(tua, ctypes.POINTER(ctypes.c_int64)),
                   srv_chunk_begin=int(srv_chunk_begin), srv_chunk_end=int(srv_chunk_end),
-                  defer_sync_writes=1 if defer_sync_writes else 0)
+                  defer_sync_writes=1 if defer_sync_writes else 0,
+                  algorithm=ALGORITHMS[algorithm])
     return cfg, (seg, tva, tua)
 
 
@@ -171,10 +175,10 @@ def zo_plan_chunks(seg_off, chunk):
 
 def zo_adam_init(cfg_kwargs, state, stream=None):
     cfg, keep = make_config(**cfg_kwargs)
-    st = _State(**{k: (state[k].data_ptr() if state[k] is not None else None)
-                   for k in ("x", "m", "v", "u", "err", "srv_err", "anchor")})
-    for k in ("x", "m", "v", "u", "err", "srv_err", "anchor"):
-        _ptr(state[k])
+    keys = ("x", "m", "v", "u", "err", "srv_err", "anchor")
+    st = _State(**{k: (state[k].data_ptr() if state.get(k) is not None else None) for k in keys})
+    for k in keys:
+        _ptr(state.get(k))
     h = ctypes.c_void_p()
     rc = lib().zo_adam_init(ctypes.byref(h), ctypes.byref(cfg), ctypes.byref(st), _stream(stream))
     if rc != ZO_OK:
@@ -208,6 +212,10 @@ def zo_sync_update(h, t, srv_packed, srv_scales, gbar=None):
 
 def zo_variance_update(h, t, gbar):
     _call(h, "zo_variance_update", int(t), _ptr(gbar))
+
+
+def zo_fullprec_step(h, t, gamma, gbar):
+    _call(h, "zo_fullprec_step", int(t), float(gamma), _ptr(gbar))
 
 
 def zo_materialize(h):
@@ -264,11 +272,12 @@ class ZoAdam:
     default)."""
 
     def __init__(self, *, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), state,
-                 srv_chunk_begin=0, srv_chunk_end=-1, defer_sync_writes=False, stream=None):
+                 srv_chunk_begin=0, srv_chunk_end=-1, defer_sync_writes=False,
+                 algorithm="zero-one", stream=None):
         self.cfg = dict(beta1=beta1, beta2=beta2, eps=eps, world=world, chunk=chunk,
                         seg_off=list(seg_off), tv=list(tv), tu=list(tu),
                         srv_chunk_begin=srv_chunk_begin, srv_chunk_end=srv_chunk_end,
-                        defer_sync_writes=defer_sync_writes)
+                        defer_sync_writes=defer_sync_writes, algorithm=algorithm)
         self.state = state
         self.h = zo_adam_init(self.cfg, state, stream)
 
@@ -304,12 +313,17 @@ class ZoAdam:
     def variance_update(self, t, gbar):
         zo_variance_update(self.h, t, gbar)
 
+    def fullprec_step(self, t, gamma, gbar):
+        zo_fullprec_step(self.h, t, gamma, gbar)
+
     def materialize(self):
         zo_materialize(self.h)
 
     def current(self, name):
         """The tensor holding state `name` now (x may live in the anchor after a
         deferred sync; u then reads as zeros)."""
+        if self.cfg["algorithm"] != "zero-one":
+            return self.state[name]
         xp, uz = zo_state_location(self.h)
         if name == "x" and xp == self.state["anchor"].data_ptr():
             return self.state["anchor"]

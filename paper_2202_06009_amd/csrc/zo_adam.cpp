@@ -76,6 +76,10 @@ struct zo_adam {
     // the anchor (x_in_anchor) and u = 0 implicit (u_zero) until the next
     // local step writes them (or zo_materialize).
     bool defer = false, x_in_anchor = false, u_zero = false;
+    // Algorithm 4 instead of Algorithm 1; fv_gamma = gamma_t of the step whose
+    // compressed average zo_sync_update applies.
+    bool fv = false;
+    float fv_gamma = 0.0f;
     char hip_err[192] = {0};
 
     bool in_tv(int64_t s) const { return std::binary_search(tv.begin(), tv.end(), s); }
@@ -139,6 +143,10 @@ int zo_config_check(const zo_config *cfg)
     if (cfg->ntv < 0 || cfg->ntu < 0) return ZO_EINVAL;
     if (cfg->ntv && (!cfg->tv || !strictly_increasing(cfg->tv, cfg->ntv))) return ZO_EINVAL;
     if (cfg->ntu && (!cfg->tu || !strictly_increasing(cfg->tu, cfg->ntu))) return ZO_EINVAL;
+    if (cfg->algorithm != ZO_ALG_ZERO_ONE_ADAM && cfg->algorithm != ZO_ALG_FROZEN_VARIANCE)
+        return ZO_EINVAL;
+    if (cfg->algorithm == ZO_ALG_FROZEN_VARIANCE && (cfg->ntu != 0 || cfg->defer_sync_writes))
+        return ZO_EINVAL;
     const int64_t nch = zo_plan_num_chunks(cfg->nseg, cfg->seg_off, cfg->chunk);
     const int64_t end = cfg->srv_chunk_end < 0 ? nch : cfg->srv_chunk_end;
     if (cfg->srv_chunk_begin < 0 || cfg->srv_chunk_begin > end || end > nch) return ZO_EINVAL;
@@ -152,10 +160,12 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
     int rc = zo_config_check(cfg);
     if (rc) return rc;
     if (!st) return ZO_EINVAL;
-    const float *ptrs[] = {st->x, st->m, st->v, st->u, st->err, st->srv_err, st->anchor};
-    for (const float *p : ptrs) {
-        if (cfg->n > 0 && !p) return ZO_EINVAL;
-        if (!aligned(p, 16)) return ZO_EALIGN;
+    const bool fv = cfg->algorithm == ZO_ALG_FROZEN_VARIANCE;
+    const float *ptrs[] = {st->x, st->m, st->v, st->err, st->srv_err, st->u, st->anchor};
+    for (int i = 0; i < 7; ++i) {
+        const bool needed = i < 5 || !fv;  // Algorithm 4 has no buffer u and no anchor
+        if (cfg->n > 0 && needed && !ptrs[i]) return ZO_EINVAL;
+        if (!aligned(ptrs[i], 16)) return ZO_EALIGN;
     }
 
     zo_adam *h = new (std::nothrow) zo_adam();
@@ -174,6 +184,7 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
     h->tv.assign(cfg->tv, cfg->tv + cfg->ntv);
     h->tu.assign(cfg->tu, cfg->tu + cfg->ntu);
     h->defer = cfg->defer_sync_writes != 0;
+    h->fv = fv;
 
     h->nchunks = zo_plan_num_chunks(cfg->nseg, cfg->seg_off, cfg->chunk);
     std::vector<int64_t> len64;
@@ -237,10 +248,12 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
         const size_t fb = (size_t)h->n * sizeof(float);
         hipError_t es[6] = {
             hipMemsetAsync(st->m, 0, fb, stream), hipMemsetAsync(st->v, 0, fb, stream),
-            hipMemsetAsync(st->u, 0, fb, stream), hipMemsetAsync(st->err, 0, fb, stream),
+            fv ? hipSuccess : hipMemsetAsync(st->u, 0, fb, stream),
+            hipMemsetAsync(st->err, 0, fb, stream),
             h->e1 > h->e0 ? hipMemsetAsync(st->srv_err, 0, (size_t)(h->e1 - h->e0) * 4, stream)
                           : hipSuccess,
-            hipMemcpyAsync(st->anchor, st->x, fb, hipMemcpyDeviceToDevice, stream)};
+            fv ? hipSuccess
+               : hipMemcpyAsync(st->anchor, st->x, fb, hipMemcpyDeviceToDevice, stream)};
         for (hipError_t e : es) {
             if (e != hipSuccess) {
                 rc = h->hip_fail(e);
@@ -280,7 +293,7 @@ static bool bad_gamma(float g) { return !(g > 0.0f) || !std::isfinite(g); }
 
 int zo_local_step(zo_adam *h, int64_t t, float gamma, const float *g, const float *gbar)
 {
-    if (!h) return ZO_EINVAL;
+    if (!h || h->fv) return ZO_EINVAL;
     if (h->n > 0 && !g) return ZO_EINVAL;
     if (bad_gamma(gamma)) return ZO_EINVAL;
     if (!aligned(g, 16) || !aligned(gbar, 16)) return ZO_EALIGN;
@@ -311,6 +324,19 @@ int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const float *g, uint
     if (h->nchunks > 0 && (!packed0 || !scales0)) return ZO_EINVAL;
     if (!aligned(g, 16)) return ZO_EALIGN;
     if (!aligned(packed0, 8) || !aligned(scales0, 4)) return ZO_EALIGN;
+    if (h->fv) {
+        // Algorithm 4, t outside T_v: compress the gradient itself (a = g + delta)
+        if (h->n > 0 && !g) return ZO_EINVAL;
+        if (bad_gamma(gamma)) return ZO_EINVAL;
+        if (t != h->t || h->phase != PH_IDLE || h->in_tv(t)) return ZO_ESTATE;
+        zo::Scalars s = h->sc;
+        hipError_t e = zo::launch_sync1(h->geo, false, false, nullptr, nullptr, g, h->st.err,
+                                        h->ch, h->nchunks, packed0, scales0, s, h->stream);
+        if (e != hipSuccess) return h->hip_fail(e);
+        h->fv_gamma = gamma;
+        h->phase = PH_COMPRESSED;
+        return ZO_OK;
+    }
     if (t != h->t || !h->in_tu(t)) return ZO_ESTATE;
     const bool fused = g != nullptr;
     if (fused) {
@@ -358,6 +384,16 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
     if (!aligned(srv_packed, 8) || !aligned(srv_scales, 4) || !aligned(gbar, 16))
         return ZO_EALIGN;
     if (t != h->t || h->phase != PH_AVERAGED) return ZO_ESTATE;
+    if (h->fv) {
+        if (gbar) return ZO_EINVAL;
+        zo::Scalars s = h->sc;
+        s.gamma = h->fv_gamma;
+        hipError_t e = zo::launch_fv_apply(srv_packed, srv_scales, h->ch, h->nchunks, h->st.x,
+                                           h->st.m, h->st.v, s, h->chunk, h->stream);
+        if (e != hipSuccess) return h->hip_fail(e);
+        h->finish_step();
+        return ZO_OK;
+    }
     const bool tv = h->in_tv(t);
     if (gbar && !tv) return ZO_EINVAL;
     // the deferred kernel reads the anchor, which holds x_{t'} in both cases
@@ -374,9 +410,24 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
     return ZO_OK;
 }
 
+int zo_fullprec_step(zo_adam *h, int64_t t, float gamma, const float *gbar)
+{
+    if (!h || !h->fv) return ZO_EINVAL;
+    if (h->n > 0 && !gbar) return ZO_EINVAL;
+    if (bad_gamma(gamma)) return ZO_EINVAL;
+    if (!aligned(gbar, 16)) return ZO_EALIGN;
+    if (t != h->t || h->phase != PH_IDLE || !h->in_tv(t)) return ZO_ESTATE;
+    zo::Scalars s = h->sc;
+    s.gamma = gamma;
+    hipError_t e = zo::launch_fv_full(gbar, h->st.x, h->st.m, h->st.v, h->n, s, h->stream);
+    if (e != hipSuccess) return h->hip_fail(e);
+    h->finish_step();
+    return ZO_OK;
+}
+
 int zo_variance_update(zo_adam *h, int64_t t, const float *gbar)
 {
-    if (!h) return ZO_EINVAL;
+    if (!h || h->fv) return ZO_EINVAL;
     if (h->n > 0 && !gbar) return ZO_EINVAL;
     if (!aligned(gbar, 16)) return ZO_EALIGN;
     if (t != h->t || h->phase != PH_VAR_PENDING) return ZO_ESTATE;
@@ -396,7 +447,7 @@ int zo_state_location(const zo_adam *h, float **x_now, int32_t *u_is_zero)
 
 int zo_materialize(zo_adam *h)
 {
-    if (!h) return ZO_EINVAL;
+    if (!h || h->fv) return ZO_EINVAL;
     if (h->phase != PH_IDLE) return ZO_ESTATE;
     if (h->x_in_anchor && h->n > 0) {
         hipError_t e = zo::launch_copy(h->st.anchor, h->st.x, h->n, true, h->stream);

@@ -51,6 +51,13 @@ hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const float *gbar,
                         float gsum, const Scalars &s, int chunk, hipStream_t st);
+// Algorithm 4: the full-precision step (t in T_v) and the step from the
+// server's compressed average (t outside T_v).
+hipError_t launch_fv_full(const float *gbar, float *x, float *m, float *v, int64_t n,
+                          const Scalars &s, hipStream_t st);
+hipError_t launch_fv_apply(const uint64_t *srv_packed, const float *srv_scales, const Chunks &ch,
+                           int64_t nchunks, float *x, float *m, const float *v, const Scalars &s,
+                           int chunk, hipStream_t st);
 hipError_t launch_copy(const float *src, float *dst, int64_t n, bool nt, hipStream_t st);
 
 // Streams of the HBM-mix diagnostic: up to 6 read and 4 write arrays.

@@ -681,6 +681,21 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
 
 // DEFER: only m and the anchor are written; the new model is the new anchor
 // and u is +0, both left implicit until the next local step writes them.
+// The chunk c and the offset e (a multiple of 4) in it of this thread's
+// float4; false when the thread has none.
+__device__ __forceinline__ bool chunk_slot(Chunks ch, int64_t nchunks, int bpc, int lb,
+                                           int64_t &c, int &e)
+{
+    if (bpc > 1) {
+        c = (int64_t)blockIdx.x / bpc;
+        e = 1024 * (int)(blockIdx.x - c * bpc) + 4 * (int)threadIdx.x;
+    } else {
+        c = (int64_t)blockIdx.x * (256 / lb) + threadIdx.x / lb;
+        e = 4 * (int)(threadIdx.x % lb);
+    }
+    return c < nchunks && e < ch.len[c];
+}
+
 template <bool VAR, bool DEFER>
 __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_packed32,
                                                const float *__restrict__ srv_scales, Chunks ch,
@@ -693,16 +708,7 @@ __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_
 {
     int64_t c;
     int e;
-    if (bpc > 1) {
-        c = (int64_t)blockIdx.x / bpc;
-        e = 1024 * (int)(blockIdx.x - c * bpc) + 4 * (int)threadIdx.x;
-    } else {
-        c = (int64_t)blockIdx.x * (256 / lb) + threadIdx.x / lb;
-        e = 4 * (int)(threadIdx.x % lb);
-    }
-    if (c >= nchunks) return;
-    const int len = ch.len[c];
-    if (e >= len) return;
+    if (!chunk_slot(ch, nchunks, bpc, lb, c, e)) return;
     const int64_t i4 = (ch.start[c] + e) >> 2;
     const float sc = srv_scales[c];
     const uint32_t bits = srv_packed32[2 * ch.word[c] + (e >> 5)] >> (e & 31);
@@ -724,6 +730,72 @@ __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_
         stnt(u, i4, f4v{0.f, 0.f, 0.f, 0.f});
     }
     if (VAR) stnt(v, i4, nv);
+}
+
+// ---------------------------------------------------------------------------
+// Algorithm 4 (frozen variance, compressed gradients; 1-bit Adam when T_v is a
+// prefix): one step given the averaged gradient gbar, in the listing's order
+//   v' = beta2 v + (1 - beta2) gbar^2 (t in T_v only);  m' = beta1 m + (1 - beta1) gbar;
+//   x' = x - gamma m / sqrt(v + eps)   (the model line uses m_t and v_t)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ void fv_elem(float gb, float &x, float &m, float &v, bool full,
+                                        const Scalars &s)
+{
+    const float v_old = v, m_old = m;
+    if (full) v = var_elem(v_old, gb, s);
+    m = s.b1 * m_old + s.c1 * gb;
+    const float step = s.gamma * m_old;
+    const float den = sqrtf(v_old + s.eps);
+    x = x - step / den;
+}
+
+// t in T_v: gbar is the full-precision average.  One float4 per thread.
+__global__ __launch_bounds__(256) void k_fv_full(const float *__restrict__ gbar,
+                                                 float *__restrict__ x, float *__restrict__ m,
+                                                 float *__restrict__ v, int64_t n4, Scalars s)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n4) return;
+    const f4v gb = ldnt(gbar, i);
+    f4v xx = ldnt(x, i), mm = ldnt(m, i), vv = ldnt(v, i);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        float xc = xx[q], mc = mm[q], vc = vv[q];
+        fv_elem(gb[q], xc, mc, vc, true, s);
+        xx[q] = xc;
+        mm[q] = mc;
+        vv[q] = vc;
+    }
+    stnt(x, i, xx);
+    stnt(m, i, mm);
+    stnt(v, i, vv);
+}
+
+// t outside T_v: gbar = sigma * s of the server's packed words (v kept).
+__global__ __launch_bounds__(256) void k_fv_apply(const uint32_t *__restrict__ srv_packed32,
+                                                  const float *__restrict__ srv_scales, Chunks ch,
+                                                  int64_t nchunks, int bpc, int lb,
+                                                  float *__restrict__ x, float *__restrict__ m,
+                                                  const float *__restrict__ v, Scalars s)
+{
+    int64_t c;
+    int e;
+    if (!chunk_slot(ch, nchunks, bpc, lb, c, e)) return;
+    const int64_t i4 = (ch.start[c] + e) >> 2;
+    const float sc = srv_scales[c];
+    const uint32_t bits = srv_packed32[2 * ch.word[c] + (e >> 5)] >> (e & 31);
+    const f4v vv = ldnt(v, i4);
+    f4v xx = ldnt(x, i4), mm = ldnt(m, i4);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        float xc = xx[q], mc = mm[q], vc = vv[q];
+        fv_elem(((bits >> q) & 1u) ? sc : -sc, xc, mc, vc, false, s);
+        xx[q] = xc;
+        mm[q] = mc;
+    }
+    stnt(x, i4, xx);
+    stnt(m, i4, mm);
 }
 
 // dst = +0, one float4 per thread (u after a deferred reset).
@@ -987,6 +1059,45 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
     }
 }
 
+// Grid of the chunk-mapped elementwise kernels (see chunk_slot): bpc
+// 256-thread workgroups per chunk of more than 1024 elements, else several
+// chunks of lb lanes per workgroup.
+static int64_t chunk_slots(int chunk, int64_t nchunks, int &bpc, int &lb)
+{
+    const int lanes = (chunk + 3) / 4;
+    if (lanes > 256) {
+        bpc = (lanes + 255) / 256;
+        lb = 256;
+        return nchunks * bpc;
+    }
+    bpc = 1;
+    lb = next_pow2(lanes);
+    return (nchunks + (256 / lb) - 1) / (256 / lb);
+}
+
+hipError_t launch_fv_full(const float *gbar, float *x, float *m, float *v, int64_t n,
+                          const Scalars &s, hipStream_t st)
+{
+    const int64_t n4 = n / 4;
+    if (n4 == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_fv_full, dim3(grid_for(n4, 256)), dim3(256), 0, st, gbar, x, m, v, n4,
+                       s);
+    return hipGetLastError();
+}
+
+hipError_t launch_fv_apply(const uint64_t *srv_packed, const float *srv_scales, const Chunks &ch,
+                           int64_t nchunks, float *x, float *m, const float *v, const Scalars &s,
+                           int chunk, hipStream_t st)
+{
+    if (nchunks == 0) return hipSuccess;
+    int bpc, lb;
+    const int64_t grid = chunk_slots(chunk, nchunks, bpc, lb);
+    hipLaunchKernelGGL(k_fv_apply, dim3((unsigned)grid), dim3(256), 0, st,
+                       reinterpret_cast<const uint32_t *>(srv_packed), srv_scales, ch, nchunks,
+                       bpc, lb, x, m, v, s);
+    return hipGetLastError();
+}
+
 hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const float *gbar,
@@ -994,18 +1105,8 @@ hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_
 {
     (void)geo;
     if (nchunks == 0) return hipSuccess;
-    const int lanes = (chunk + 3) / 4;
     int bpc, lb;
-    int64_t grid;
-    if (lanes > 256) {
-        bpc = (lanes + 255) / 256;
-        lb = 256;
-        grid = nchunks * bpc;
-    } else {
-        bpc = 1;
-        lb = next_pow2(lanes);
-        grid = (nchunks + (256 / lb) - 1) / (256 / lb);
-    }
+    const int64_t grid = chunk_slots(chunk, nchunks, bpc, lb);
     const uint32_t *p32 = reinterpret_cast<const uint32_t *>(srv_packed);
     const dim3 g3((unsigned)grid), b3(256);
     if (var && defer)

@@ -121,7 +121,14 @@ class Workload:
                 break
         return s
 
+    @property
+    def algorithm(self):
+        return self.extra.get("algorithm", "zero-one")
+
     def peer_scale_base(self, t):
+        if self.algorithm == "frozen-variance":
+            # the compressed quantity is the gradient itself: E|g| = 0.8 sigma
+            return np.float32(0.8 * self.sigma_g)
         return np.float32(self.interval_gamma_sum(t) * 0.18 * self.sigma_g)
 
 
@@ -178,6 +185,28 @@ def gpt2_1p5b():
 
 ALL = {"tiny": tiny, "tiny-alt": lambda: tiny(True), "bert-base": bert_base,
        "bert-large": bert_large, "resnet50": resnet50, "gpt2-1.5b": gpt2_1p5b}
+
+
+def one_bit(base, t0):
+    """The same shard run by Algorithm 4 as 1-bit Adam: full-precision steps
+    (variance updates) for t < t0, then compressed gradients with the variance
+    frozen, no local steps."""
+    def make():
+        wl = ALL[base]()
+        return Workload(name=f"{base}-1bit", seg_off=wl.seg_off, world=wl.world, chunk=wl.chunk,
+                        steps=wl.steps, tv=list(range(min(t0, wl.steps))), tu=[],
+                        gammas=wl.gammas, sigma_g=wl.sigma_g,
+                        outlier_per_mille=wl.outlier_per_mille,
+                        outlier_factor=wl.outlier_factor, sigma_x=wl.sigma_x, beta1=wl.beta1,
+                        beta2=wl.beta2, eps=wl.eps,
+                        notes=f"1-bit Adam on the {base} shard, full-precision stage of {t0} steps",
+                        extra={"algorithm": "frozen-variance"})
+    return make
+
+
+for _b, _t0 in (("tiny", 6), ("bert-base", 16), ("bert-large", 16), ("resnet50", 16),
+                ("gpt2-1.5b", 32)):
+    ALL[f"{_b}-1bit"] = one_bit(_b, _t0)
 
 
 def get(name):

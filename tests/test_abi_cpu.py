@@ -70,6 +70,9 @@ def _cfg(**over):
     ({"srv_chunk_begin": 1, "srv_chunk_end": 3}, zo.ZO_OK),
     ({"srv_chunk_begin": 3, "srv_chunk_end": 5}, zo.ZO_EINVAL),
     ({"srv_chunk_begin": 2, "srv_chunk_end": 1}, zo.ZO_EINVAL),
+    ({"algorithm": "frozen-variance", "tu": []}, zo.ZO_OK),
+    ({"algorithm": "frozen-variance"}, zo.ZO_EINVAL),            # T_u must be empty
+    ({"algorithm": "frozen-variance", "tu": [], "defer_sync_writes": True}, zo.ZO_EINVAL),
 ])
 def test_config_validation(over, code):
     assert zo.zo_config_check(**_cfg(**over)) == code
@@ -126,3 +129,14 @@ def test_diag_stream_validates_before_touching_the_device():
     assert lib.zo_diag_stream(arr, 1, arr, 5, 16, None) == zo.ZO_EINVAL   # too many writes
     assert lib.zo_diag_stream(arr, 1, arr, 1, 6, None) == zo.ZO_EINVAL    # n not a multiple of 4
     assert lib.zo_diag_stream(arr, 1, arr, 1, 16, None) == zo.ZO_EINVAL   # null buffers
+
+
+def test_unknown_algorithm_is_rejected():
+    cfg, keep = zo.make_config(**_cfg())
+    cfg.algorithm = 7
+    assert zo.lib().zo_config_check(ctypes.byref(cfg)) == zo.ZO_EINVAL
+
+
+def test_fullprec_step_rejects_null_handle():
+    assert zo.lib().zo_fullprec_step(None, 0, 1e-4, None) == zo.ZO_EINVAL
+
