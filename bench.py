@@ -112,39 +112,41 @@ def measured_traffic(kernel, mode):
     return t["kernels"][kernel]["traffic_bytes"]
 
 
-def algorithmic_bytes_fv(d, nchunks, nwords, W):
-    """Algorithm 4: bytes each kernel must move per launch."""
+def algorithmic_bytes_fv(d, nchunks, nwords, W, gbytes=4):
+    """Algorithm 4: bytes each kernel must move per launch (gbytes: bytes per
+    gradient element)."""
     pk = 8 * nwords
     sc = 4 * nchunks
     return {
         # reads gbar, x, m, v; writes x, m, v
-        "fv_full": 28 * d,
+        "fv_full": (24 + gbytes) * d,
         # reads g, err; writes err, own packed words, own scales
-        "sync1": 12 * d + pk + sc,
+        "sync1": (8 + gbytes) * d + pk + sc,
         "srv": W * (pk + sc) + 8 * d + pk + sc,
         # reads server words + scales, x, m, v; writes x, m
         "fv_apply": pk + sc + 20 * d,
     }
 
 
-def algorithmic_bytes(d, nchunks, nwords, W, deferred=True):
+def algorithmic_bytes(d, nchunks, nwords, W, deferred=True, gbytes=4):
     """Bytes each kernel must move per launch: every state read once and
-    written once, packed words and per-chunk scales included.  With deferred
-    sync writes the local step after a sync reads x from the anchor and does
-    not read u, and the reconstruction writes neither x nor u."""
+    written once, packed words and per-chunk scales included (gbytes: bytes
+    per gradient element of g and gbar).  With deferred sync writes the local
+    step after a sync reads x from the anchor and does not read u, and the
+    reconstruction writes neither x nor u."""
     pk = 8 * nwords
     sc = 4 * nchunks
     return {
         # reads g, m, x, v, u (eager only), gbar; writes m, x, u, v
-        "local+var": (36 if deferred else 40) * d,
+        "local+var": ((28 if deferred else 32) + 2 * gbytes) * d,
         # reads g, m, u, err; writes err, own packed words, own scales
-        "sync1": 20 * d + pk + sc,
+        "sync1": (16 + gbytes) * d + pk + sc,
         # reads W packed buffers + W scale rows + server error;
         # writes server error, server packed words, server scales
         "srv": W * (pk + sc) + 8 * d + pk + sc,
         # reads server words + scales, v, anchor, gbar; writes m, anchor, v,
         # and x, u (eager only)
-        "recon+var": pk + sc + (24 if deferred else 32) * d,
+        "recon+var": pk + sc + ((20 if deferred else 28) + gbytes) * d,
     }
 
 
@@ -239,6 +241,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager-sync-writes", action="store_true",
                     help="the reconstruction writes x and u at every sync")
+    ap.add_argument("--grad-dtype", choices=("f32", "f16", "bf16"), default="f32",
+                    help="element type of the gradient inputs g and gbar")
     ap.add_argument("--algorithm", choices=("zero-one", "frozen-variance"), default="zero-one",
                     help="frozen-variance: Algorithm 4 (1-bit Adam's compression stage), one "
                          "full-precision and one compressed step per bench step")
@@ -249,6 +253,8 @@ def main():
     args = ap.parse_args()
     fv = args.algorithm == "frozen-variance"
     mode = "frozen-variance" if fv else ("eager" if args.eager_sync_writes else "deferred")
+    if args.grad_dtype != "f32":
+        mode += f"/{args.grad_dtype}"
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], TRAFFIC_FILE, mode)
         return
@@ -289,6 +295,8 @@ def main():
     scales = torch.empty((W, nchunks), **f32)
     srv_packed = torch.empty(nwords, dtype=torch.int64, device=dev)
     srv_scales = torch.empty(nchunks, **f32)
+    gdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[args.grad_dtype]
+    gbytes = torch.empty(0, dtype=gdt).element_size()
 
     ks = C.ksigma(wl.sigma_g)
     synth.normal_dev(state["x"], 0, synth.key(0, C.STREAM_X, 0), C.ksigma(wl.sigma_x))
@@ -296,6 +304,7 @@ def main():
                      wl.outlier_factor)
     synth.normal_dev(gb, 0, synth.key(0, C.STREAM_GBAR, 0), ks, wl.outlier_per_mille,
                      wl.outlier_factor)
+    g_in, gb_in = (g, gb) if gdt == torch.float32 else (g.to(gdt), gb.to(gdt))
     # peers compress u (two steps of gamma m) under Algorithm 1, g under Algorithm 4
     base = 0.8 * wl.sigma_g if fv else 2 * 1e-4 * 0.18 * wl.sigma_g
     for w in range(1, W):
@@ -306,26 +315,27 @@ def main():
     if fv:
         opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=W, chunk=wl.chunk,
                         seg_off=wl.seg_off, tv=list(range(0, total_steps, 2)), tu=[],
-                        state=state, algorithm="frozen-variance")
+                        state=state, algorithm="frozen-variance", grad_dtype=args.grad_dtype)
         names = ("fv_full", "sync1", "srv", "fv_apply")
     else:
         opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=W, chunk=wl.chunk,
                         seg_off=wl.seg_off, tv=list(range(total_steps)),
                         tu=list(range(1, total_steps, 2)), state=state,
-                        defer_sync_writes=not args.eager_sync_writes)
+                        defer_sync_writes=not args.eager_sync_writes,
+                        grad_dtype=args.grad_dtype)
         names = ("local+var", "sync1", "srv", "recon+var")
     torch.cuda.synchronize()
     gamma = 1e-4
 
     def bench_step(k, ev=None):
         t = 2 * k
-        first = (lambda: opt.fullprec_step(t, gamma, gb)) if fv else \
-            (lambda: opt.local_step(t, gamma, g, gb))
+        first = (lambda: opt.fullprec_step(t, gamma, gb_in)) if fv else \
+            (lambda: opt.local_step(t, gamma, g_in, gb_in))
         calls = (
             first,
-            lambda: opt.compress_pack_ef(t + 1, gamma, g, packed[0], scales[0]),
+            lambda: opt.compress_pack_ef(t + 1, gamma, g_in, packed[0], scales[0]),
             lambda: opt.unpack_average(t + 1, packed, scales, srv_packed, srv_scales),
-            lambda: opt.sync_update(t + 1, srv_packed, srv_scales, None if fv else gb),
+            lambda: opt.sync_update(t + 1, srv_packed, srv_scales, None if fv else gb_in),
         )
         for i, call in enumerate(calls):
             if ev is not None:
@@ -351,12 +361,15 @@ def main():
                   / args.steps for i, n in enumerate(names)}
     inexact = opt.inexact_chunks()
     opt.close()
-    mix = stream_mix_ceilings(zo, torch, state, g, gb, d, mode)
+    # (the diagnostic streams binary32 arrays: no like-for-like mix for 16-bit gradients)
+    mix = stream_mix_ceilings(zo, torch, state, g, gb, d, mode) \
+        if args.grad_dtype == "f32" else None
 
     ms_per_step = wall * 1000.0 / args.steps
     value = 2.0 * d / (ms_per_step / 1000.0)
-    bytes_ = algorithmic_bytes_fv(d, nchunks, nwords, W) if fv else \
-        algorithmic_bytes(d, nchunks, nwords, W, deferred=not args.eager_sync_writes)
+    bytes_ = algorithmic_bytes_fv(d, nchunks, nwords, W, gbytes) if fv else \
+        algorithmic_bytes(d, nchunks, nwords, W, deferred=not args.eager_sync_writes,
+                          gbytes=gbytes)
     kernels = {n: {"ms": round(per_kernel[n], 4),
                    "gb_per_launch": round(bytes_[n] / 1e9, 3),
                    "gbs": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0), 1),
@@ -383,7 +396,7 @@ def main():
                        "Algorithm 4: one full-precision and one compressed step per bench step"
                        if fv else "one local+variance step and one sync+variance step per "
                                   "bench step"),
-                   "algorithm": args.algorithm,
+                   "algorithm": args.algorithm, "grad_dtype": args.grad_dtype,
                    "params": d, "segments": wl.nseg, "world": W, "chunk": wl.chunk,
                    "chunks": nchunks, "server": "single (all chunks)",
                    "sync_writes": None if fv else ("eager" if args.eager_sync_writes

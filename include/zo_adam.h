@@ -10,9 +10,13 @@
  *
  * Conventions shared by every entry point
  *   - Device pointers are caller-owned HIP device allocations.  Float vectors
- *     of shard length (state, g, gbar, avg_debug) must be 16-byte aligned,
+ *     of shard length (state, avg_debug, and g and gbar when binary32) must
+ *     be 16-byte aligned, binary16 / bfloat16 g and gbar 8-byte aligned,
  *     packed word buffers 8-byte aligned, scale buffers 4-byte aligned
  *     (ZO_EALIGN otherwise).  The library never frees or reallocates them.
+ *   - The gradient inputs g and gbar have the element type grad_dtype of
+ *     the configuration (binary32 by default; binary16 or bfloat16, as in
+ *     the paper's FP16 training, are widened exactly to binary32 on load).
  *   - Every call validates all of its arguments on the host before enqueueing
  *     anything; a rejected call returns a negative status and changes nothing.
  *   - Calls are asynchronous on the stream given to zo_adam_init (or
@@ -59,6 +63,9 @@ enum {
     ZO_ENOMEM = -5    /* host or device allocation failed in zo_adam_init */
 };
 
+/* Element types of the gradient inputs (zo_config.grad_dtype). */
+enum { ZO_DTYPE_F32 = 0, ZO_DTYPE_F16 = 1, ZO_DTYPE_BF16 = 2 };
+
 /* Algorithms (zo_config.algorithm). */
 enum {
     ZO_ALG_ZERO_ONE_ADAM = 0,     /* Algorithm 1 with Algorithm 2 (0/1 Adam) */
@@ -101,6 +108,9 @@ typedef struct zo_adam zo_adam;   /* opaque handle */
  *                  t, zo_compress_pack_ef (with the gradient), zo_unpack_average
  *                  and zo_sync_update (gbar = NULL).  st.u and st.anchor are
  *                  unused and may be NULL.
+ *   grad_dtype     ZO_DTYPE_F32 (default 0), ZO_DTYPE_F16 or ZO_DTYPE_BF16:
+ *                  the element type of every g and gbar argument.  All
+ *                  arithmetic stays binary32 (16-bit values widen exactly).
  */
 typedef struct zo_config {
     float beta1, beta2, eps;
@@ -116,6 +126,7 @@ typedef struct zo_config {
     int64_t srv_chunk_begin, srv_chunk_end;
     int32_t defer_sync_writes;
     int32_t algorithm;
+    int32_t grad_dtype;
 } zo_config;
 
 /*
@@ -154,8 +165,8 @@ int zo_set_stream(zo_adam *h, hipStream_t stream);
  * The momentum used in the model and buffer lines is the fresh m' (the literal
  * subscript t would freeze the momentum when every step synchronises).
  *   gamma   learning rate gamma_t > 0, finite.
- *   g       device float[n], this worker's stochastic gradient g_t.
- *   gbar    NULL, or device float[n] with the full-precision average gradient
+ *   g       device [n] of grad_dtype, this worker's stochastic gradient g_t.
+ *   gbar    NULL, or device [n] of grad_dtype with the full-precision average gradient
  *           of step t when t is in T_v and t is not in T_u: the variance line
  *           v <- beta2 v + (1 - beta2) gbar^2 is then fused (v_t is used above
  *           before it is overwritten).  Passing gbar when t is not in T_v, or
@@ -164,7 +175,7 @@ int zo_set_stream(zo_adam *h, hipStream_t stream);
  * due).  At t in T_u it is the unfused first half of a sync step:
  * zo_compress_pack_ef with g = NULL must follow.
  */
-int zo_local_step(zo_adam *h, int64_t t, float gamma, const float *g, const float *gbar);
+int zo_local_step(zo_adam *h, int64_t t, float gamma, const void *g, const void *gbar);
 
 /*
  * zo_compress_pack_ef -- worker half of Algorithm 2 applied to the buffer
@@ -182,7 +193,7 @@ int zo_local_step(zo_adam *h, int64_t t, float gamma, const float *g, const floa
  *   packed0  device uint64[words]: this worker's packed signs (slot 0).
  *   scales0  device float[nchunks]: this worker's scales (slot 0).
  */
-int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const float *g,
+int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const void *g,
                         uint64_t *packed0, float *scales0);
 
 /*
@@ -223,7 +234,7 @@ int zo_unpack_average(zo_adam *h, int64_t t, const uint64_t *packed, const float
  * writes them; gbar must be NULL.
  */
 int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const float *srv_scales,
-                   const float *gbar);
+                   const void *gbar);
 
 /*
  * zo_fullprec_step -- ZO_ALG_FROZEN_VARIANCE, t in T_v: one step of
@@ -233,14 +244,14 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
  * ZO_EINVAL on a ZO_ALG_ZERO_ONE_ADAM handle; ZO_ESTATE if t is not the next
  * step or not in T_v.
  */
-int zo_fullprec_step(zo_adam *h, int64_t t, float gamma, const float *gbar);
+int zo_fullprec_step(zo_adam *h, int64_t t, float gamma, const void *gbar);
 
 /*
  * zo_variance_update -- the variance line of Algorithm 1 for t in T_v when it
  * was not fused: v <- beta2 v + (1 - beta2) gbar^2, after the other calls of
  * step t.  gbar: device float[n], the full-precision AllReduce output.
  */
-int zo_variance_update(zo_adam *h, int64_t t, const float *gbar);
+int zo_variance_update(zo_adam *h, int64_t t, const void *gbar);
 
 /*
  * zo_materialize -- with defer_sync_writes, write out what the last

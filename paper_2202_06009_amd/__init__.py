@@ -15,6 +15,8 @@ LIB_PATH = os.path.join(HERE, "libzoadam.so")
 
 ZO_OK, ZO_EINVAL, ZO_EALIGN, ZO_ESTATE, ZO_EHIP, ZO_ENOMEM = 0, -1, -2, -3, -4, -5
 ZO_ALG_ZERO_ONE_ADAM, ZO_ALG_FROZEN_VARIANCE = 0, 1
+ZO_DTYPE_F32, ZO_DTYPE_F16, ZO_DTYPE_BF16 = 0, 1, 2
+GRAD_DTYPES = {"f32": ZO_DTYPE_F32, "f16": ZO_DTYPE_F16, "bf16": ZO_DTYPE_BF16}
 ALGORITHMS = {"zero-one": ZO_ALG_ZERO_ONE_ADAM, "frozen-variance": ZO_ALG_FROZEN_VARIANCE}
 
 # Every function the header declares (checked by the CPU export test).
@@ -44,7 +46,8 @@ class _Config(ctypes.Structure):
                 ("ntv", ctypes.c_int32), ("tv", ctypes.POINTER(ctypes.c_int64)),
                 ("ntu", ctypes.c_int32), ("tu", ctypes.POINTER(ctypes.c_int64)),
                 ("srv_chunk_begin", ctypes.c_int64), ("srv_chunk_end", ctypes.c_int64),
-                ("defer_sync_writes", ctypes.c_int32), ("algorithm", ctypes.c_int32)]
+                ("defer_sync_writes", ctypes.c_int32), ("algorithm", ctypes.c_int32),
+                ("grad_dtype", ctypes.c_int32)]
 
 
 class _State(ctypes.Structure):
@@ -133,7 +136,8 @@ def _i64_array(values):
 
 
 def make_config(*, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), srv_chunk_begin=0,
-                srv_chunk_end=-1, defer_sync_writes=False, algorithm="zero-one"):
+                srv_chunk_end=-1, defer_sync_writes=False, algorithm="zero-one",
+                grad_dtype="f32"):
     """Build a C config; returns (struct, keepalive) -- keep both alive."""
     seg, nseg1 = _i64_array(seg_off)
     tva, ntv = _i64_array(tv)
@@ -145,7 +149,7 @@ def make_config(*, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), srv_c
                   tu=ctypes.cast(tua, ctypes.POINTER(ctypes.c_int64)),
                   srv_chunk_begin=int(srv_chunk_begin), srv_chunk_end=int(srv_chunk_end),
                   defer_sync_writes=1 if defer_sync_writes else 0,
-                  algorithm=ALGORITHMS[algorithm])
+                  algorithm=ALGORITHMS[algorithm], grad_dtype=GRAD_DTYPES[grad_dtype])
     return cfg, (seg, tva, tua)
 
 
@@ -273,11 +277,12 @@ class ZoAdam:
 
     def __init__(self, *, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), state,
                  srv_chunk_begin=0, srv_chunk_end=-1, defer_sync_writes=False,
-                 algorithm="zero-one", stream=None):
+                 algorithm="zero-one", grad_dtype="f32", stream=None):
         self.cfg = dict(beta1=beta1, beta2=beta2, eps=eps, world=world, chunk=chunk,
                         seg_off=list(seg_off), tv=list(tv), tu=list(tu),
                         srv_chunk_begin=srv_chunk_begin, srv_chunk_end=srv_chunk_end,
-                        defer_sync_writes=defer_sync_writes, algorithm=algorithm)
+                        defer_sync_writes=defer_sync_writes, algorithm=algorithm,
+                        grad_dtype=grad_dtype)
         self.state = state
         self.h = zo_adam_init(self.cfg, state, stream)
 

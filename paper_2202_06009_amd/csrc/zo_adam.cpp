@@ -80,6 +80,8 @@ struct zo_adam {
     // compressed average zo_sync_update applies.
     bool fv = false;
     float fv_gamma = 0.0f;
+    int gt = zo::GT_F32;          // element type of g and gbar
+    uintptr_t galign = 16;        // their alignment: one float4 of elements
     char hip_err[192] = {0};
 
     bool in_tv(int64_t s) const { return std::binary_search(tv.begin(), tv.end(), s); }
@@ -147,6 +149,9 @@ int zo_config_check(const zo_config *cfg)
         return ZO_EINVAL;
     if (cfg->algorithm == ZO_ALG_FROZEN_VARIANCE && (cfg->ntu != 0 || cfg->defer_sync_writes))
         return ZO_EINVAL;
+    if (cfg->grad_dtype != ZO_DTYPE_F32 && cfg->grad_dtype != ZO_DTYPE_F16 &&
+        cfg->grad_dtype != ZO_DTYPE_BF16)
+        return ZO_EINVAL;
     const int64_t nch = zo_plan_num_chunks(cfg->nseg, cfg->seg_off, cfg->chunk);
     const int64_t end = cfg->srv_chunk_end < 0 ? nch : cfg->srv_chunk_end;
     if (cfg->srv_chunk_begin < 0 || cfg->srv_chunk_begin > end || end > nch) return ZO_EINVAL;
@@ -185,6 +190,9 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
     h->tu.assign(cfg->tu, cfg->tu + cfg->ntu);
     h->defer = cfg->defer_sync_writes != 0;
     h->fv = fv;
+    h->gt = cfg->grad_dtype == ZO_DTYPE_F16 ? zo::GT_F16
+            : cfg->grad_dtype == ZO_DTYPE_BF16 ? zo::GT_BF16 : zo::GT_F32;
+    h->galign = h->gt == zo::GT_F32 ? 16 : 8;
 
     h->nchunks = zo_plan_num_chunks(cfg->nseg, cfg->seg_off, cfg->chunk);
     std::vector<int64_t> len64;
@@ -291,12 +299,12 @@ int zo_set_stream(zo_adam *h, hipStream_t stream)
 
 static bool bad_gamma(float g) { return !(g > 0.0f) || !std::isfinite(g); }
 
-int zo_local_step(zo_adam *h, int64_t t, float gamma, const float *g, const float *gbar)
+int zo_local_step(zo_adam *h, int64_t t, float gamma, const void *g, const void *gbar)
 {
     if (!h || h->fv) return ZO_EINVAL;
     if (h->n > 0 && !g) return ZO_EINVAL;
     if (bad_gamma(gamma)) return ZO_EINVAL;
-    if (!aligned(g, 16) || !aligned(gbar, 16)) return ZO_EALIGN;
+    if (!aligned(g, h->galign) || !aligned(gbar, h->galign)) return ZO_EALIGN;
     if (h->phase != PH_IDLE || t != h->t) return ZO_ESTATE;
     const bool tu = h->in_tu(t), tv = h->in_tv(t);
     if (gbar && (!tv || tu)) return ZO_EINVAL;
@@ -304,7 +312,7 @@ int zo_local_step(zo_adam *h, int64_t t, float gamma, const float *g, const floa
     s.gamma = gamma;
     const float *x_src = h->x_in_anchor ? h->st.anchor : h->st.x;
     hipError_t e = zo::launch_local(gbar != nullptr, h->u_zero, g, h->st.m, x_src, h->st.x,
-                                    h->st.v, h->st.u, gbar, h->n, s, h->stream);
+                                    h->st.v, h->st.u, gbar, h->n, s, h->gt, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     h->x_in_anchor = h->u_zero = false;
     h->gamma_sum = h->gamma_sum + gamma;
@@ -317,12 +325,12 @@ int zo_local_step(zo_adam *h, int64_t t, float gamma, const float *g, const floa
     return ZO_OK;
 }
 
-int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const float *g, uint64_t *packed0,
+int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const void *g, uint64_t *packed0,
                         float *scales0)
 {
     if (!h) return ZO_EINVAL;
     if (h->nchunks > 0 && (!packed0 || !scales0)) return ZO_EINVAL;
-    if (!aligned(g, 16)) return ZO_EALIGN;
+    if (!aligned(g, h->galign)) return ZO_EALIGN;
     if (!aligned(packed0, 8) || !aligned(scales0, 4)) return ZO_EALIGN;
     if (h->fv) {
         // Algorithm 4, t outside T_v: compress the gradient itself (a = g + delta)
@@ -331,7 +339,8 @@ int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const float *g, uint
         if (t != h->t || h->phase != PH_IDLE || h->in_tv(t)) return ZO_ESTATE;
         zo::Scalars s = h->sc;
         hipError_t e = zo::launch_sync1(h->geo, false, false, nullptr, nullptr, g, h->st.err,
-                                        h->ch, h->nchunks, packed0, scales0, s, h->stream);
+                                        h->ch, h->nchunks, packed0, scales0, s, zo::GT_F32,
+                                        h->gt, h->stream);
         if (e != hipSuccess) return h->hip_fail(e);
         h->fv_gamma = gamma;
         h->phase = PH_COMPRESSED;
@@ -350,7 +359,8 @@ int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const float *g, uint
     // (after zo_local_step at this step u has been written, so u_zero is false
     // on the unfused path)
     hipError_t e = zo::launch_sync1(h->geo, fused, fused && h->u_zero, g, h->st.m, h->st.u,
-                                    h->st.err, h->ch, h->nchunks, packed0, scales0, s, h->stream);
+                                    h->st.err, h->ch, h->nchunks, packed0, scales0, s, h->gt,
+                                    zo::GT_F32, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     if (fused) h->gamma_sum = h->gamma_sum + gamma;
     h->phase = PH_COMPRESSED;
@@ -377,11 +387,11 @@ int zo_unpack_average(zo_adam *h, int64_t t, const uint64_t *packed, const float
 }
 
 int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const float *srv_scales,
-                   const float *gbar)
+                   const void *gbar)
 {
     if (!h) return ZO_EINVAL;
     if (h->nchunks > 0 && (!srv_packed || !srv_scales)) return ZO_EINVAL;
-    if (!aligned(srv_packed, 8) || !aligned(srv_scales, 4) || !aligned(gbar, 16))
+    if (!aligned(srv_packed, 8) || !aligned(srv_scales, 4) || !aligned(gbar, h->galign))
         return ZO_EALIGN;
     if (t != h->t || h->phase != PH_AVERAGED) return ZO_ESTATE;
     if (h->fv) {
@@ -399,7 +409,8 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
     // the deferred kernel reads the anchor, which holds x_{t'} in both cases
     hipError_t e = zo::launch_recon(h->geo, gbar != nullptr, h->defer, srv_packed, srv_scales,
                                     h->ch, h->nchunks, h->st.m, h->st.x, h->st.v, h->st.u,
-                                    h->st.anchor, gbar, h->gamma_sum, h->sc, h->chunk, h->stream);
+                                    h->st.anchor, gbar, h->gamma_sum, h->sc, h->gt, h->chunk,
+                                    h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     if (h->defer) h->x_in_anchor = h->u_zero = true;
     h->gamma_sum = 0.0f;
@@ -410,28 +421,28 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
     return ZO_OK;
 }
 
-int zo_fullprec_step(zo_adam *h, int64_t t, float gamma, const float *gbar)
+int zo_fullprec_step(zo_adam *h, int64_t t, float gamma, const void *gbar)
 {
     if (!h || !h->fv) return ZO_EINVAL;
     if (h->n > 0 && !gbar) return ZO_EINVAL;
     if (bad_gamma(gamma)) return ZO_EINVAL;
-    if (!aligned(gbar, 16)) return ZO_EALIGN;
+    if (!aligned(gbar, h->galign)) return ZO_EALIGN;
     if (t != h->t || h->phase != PH_IDLE || !h->in_tv(t)) return ZO_ESTATE;
     zo::Scalars s = h->sc;
     s.gamma = gamma;
-    hipError_t e = zo::launch_fv_full(gbar, h->st.x, h->st.m, h->st.v, h->n, s, h->stream);
+    hipError_t e = zo::launch_fv_full(gbar, h->st.x, h->st.m, h->st.v, h->n, s, h->gt, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     h->finish_step();
     return ZO_OK;
 }
 
-int zo_variance_update(zo_adam *h, int64_t t, const float *gbar)
+int zo_variance_update(zo_adam *h, int64_t t, const void *gbar)
 {
     if (!h || h->fv) return ZO_EINVAL;
     if (h->n > 0 && !gbar) return ZO_EINVAL;
-    if (!aligned(gbar, 16)) return ZO_EALIGN;
+    if (!aligned(gbar, h->galign)) return ZO_EALIGN;
     if (t != h->t || h->phase != PH_VAR_PENDING) return ZO_ESTATE;
-    hipError_t e = zo::launch_var(h->st.v, gbar, h->n, h->sc, h->stream);
+    hipError_t e = zo::launch_var(h->st.v, gbar, h->n, h->sc, h->gt, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     h->finish_step();
     return ZO_OK;

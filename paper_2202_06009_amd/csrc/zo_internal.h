@@ -29,18 +29,25 @@ struct Geometry {
 
 Geometry geometry_for(int chunk);
 
+// Element type of the gradient inputs g and gbar (zo_config.grad_dtype).
+enum GradType { GT_F32 = 0, GT_F16 = 1, GT_BF16 = 2 };
+
 // Server-average algorithm.
 enum SrvAlgo { SRV_AUTO = 0, SRV_PLAIN = 1 };
 
 // uz: u is +0 and not read (a deferred reset); x_src may equal x.
-hipError_t launch_local(bool var, bool uz, const float *g, float *m, const float *x_src, float *x,
-                        float *v, float *u, const float *gbar, int64_t n, const Scalars &s,
+hipError_t launch_local(bool var, bool uz, const void *g, float *m, const float *x_src, float *x,
+                        float *v, float *u, const void *gbar, int64_t n, const Scalars &s, int gt,
                         hipStream_t st);
 hipError_t launch_zero(float *dst, int64_t n, hipStream_t st);
-hipError_t launch_var(float *v, const float *gbar, int64_t n, const Scalars &s, hipStream_t st);
-hipError_t launch_sync1(Geometry geo, bool fused, bool uz, const float *g, const float *m,
-                        const float *u, float *err, const Chunks &ch, int64_t nchunks,
-                        uint64_t *packed, float *scales, const Scalars &s, hipStream_t st);
+hipError_t launch_var(float *v, const void *gbar, int64_t n, const Scalars &s, int gt,
+                      hipStream_t st);
+// gt: element type of g (fused); ut: of u, the compressed source when not
+// fused (binary32 u, or the gradient under Algorithm 4).
+hipError_t launch_sync1(Geometry geo, bool fused, bool uz, const void *g, const float *m,
+                        const void *u, float *err, const Chunks &ch, int64_t nchunks,
+                        uint64_t *packed, float *scales, const Scalars &s, int gt, int ut,
+                        hipStream_t st);
 hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const float *scales, int W,
                       int64_t wstride, int64_t cstride, const Chunks &ch, int64_t c0,
                       int64_t nch, int64_t word0, int64_t elem0, float *srv_err,
@@ -49,12 +56,12 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
 // defer: write m and anchor only (the model stays in the anchor, u = 0 implicit).
 hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
-                        float *x, float *v, float *u, float *anchor, const float *gbar,
-                        float gsum, const Scalars &s, int chunk, hipStream_t st);
+                        float *x, float *v, float *u, float *anchor, const void *gbar,
+                        float gsum, const Scalars &s, int gt, int chunk, hipStream_t st);
 // Algorithm 4: the full-precision step (t in T_v) and the step from the
 // server's compressed average (t outside T_v).
-hipError_t launch_fv_full(const float *gbar, float *x, float *m, float *v, int64_t n,
-                          const Scalars &s, hipStream_t st);
+hipError_t launch_fv_full(const void *gbar, float *x, float *m, float *v, int64_t n,
+                          const Scalars &s, int gt, hipStream_t st);
 hipError_t launch_fv_apply(const uint64_t *srv_packed, const float *srv_scales, const Chunks &ch,
                            int64_t nchunks, float *x, float *m, const float *v, const Scalars &s,
                            int chunk, hipStream_t st);

@@ -60,6 +60,47 @@ __device__ __forceinline__ void stnt(float *p, int64_t i4, f4v v)
     __builtin_nontemporal_store(v, reinterpret_cast<f4v *>(p) + i4);
 }
 
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+
+// Four elements i4*4 .. i4*4+3 of a gradient array of element type GT
+// (binary32, or binary16 / bfloat16 widened exactly), as a float4.  The type
+// is a template argument: a run-time switch would leave loads of different
+// widths pending across a branch merge, and the compiler then waits for all
+// of them before the next load.
+template <int GT>
+__device__ __forceinline__ f4v ldg4(const void *p, int64_t i4)
+{
+    if constexpr (GT == GT_F32) {
+        return ldnt(static_cast<const float *>(p), i4);
+    } else {
+        const u2v w = __builtin_nontemporal_load(static_cast<const u2v *>(p) + i4);
+        f4v r;
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            if constexpr (GT == GT_BF16) {
+                r[2 * q] = __uint_as_float(w[q] << 16);
+                r[2 * q + 1] = __uint_as_float(w[q] & 0xFFFF0000u);
+            } else {
+                r[2 * q] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[q] & 0xFFFFu));
+                r[2 * q + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[q] >> 16));
+            }
+        }
+        return r;
+    }
+}
+
+// Calls f(integral_constant<GT>) for a run-time gradient type.
+template <class F>
+static hipError_t with_grad_type(int gt, F &&f)
+{
+    switch (gt) {
+    case GT_F32: return f(std::integral_constant<int, GT_F32>{});
+    case GT_F16: return f(std::integral_constant<int, GT_F16>{});
+    case GT_BF16: return f(std::integral_constant<int, GT_BF16>{});
+    default: return hipErrorInvalidValue;
+    }
+}
+
 // Momentum / model / buffer lines of Algorithm 1 for one element, with the
 // fresh momentum in the model and buffer lines.
 __device__ __forceinline__ void local_elem(float g, float &m, float &x, float v, float &u,
@@ -87,19 +128,19 @@ __device__ __forceinline__ float var_elem(float v, float gb, const Scalars &s)
 // synchronisation left the model there) and written to x.  UZ: u is +0
 // everywhere (reset by the last synchronisation and not yet written), so it
 // is not read.
-template <bool VAR, bool UZ>
-__global__ __launch_bounds__(256) void k_local(const float *__restrict__ g, float *__restrict__ m,
+template <bool VAR, bool UZ, int GT>
+__global__ __launch_bounds__(256) void k_local(const void *__restrict__ g, float *__restrict__ m,
                                                const float *x_src, float *x,
                                                float *__restrict__ v, float *__restrict__ u,
-                                               const float *__restrict__ gbar, int64_t n4,
+                                               const void *__restrict__ gbar, int64_t n4,
                                                Scalars s)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n4) return;
-    f4v gg = ldnt(g, i), mm = ldnt(m, i), xx = ldnt(x_src, i), vv = ldnt(v, i);
+    f4v gg = ldg4<GT>(g, i), mm = ldnt(m, i), xx = ldnt(x_src, i), vv = ldnt(v, i);
     f4v uu = UZ ? f4v{0.f, 0.f, 0.f, 0.f} : ldnt(u, i);
     f4v gb;
-    if (VAR) gb = ldnt(gbar, i);
+    if (VAR) gb = ldg4<GT>(gbar, i);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
         float mc = mm[c], xc = xx[c], uc = uu[c];
@@ -119,12 +160,13 @@ __global__ __launch_bounds__(256) void k_local(const float *__restrict__ g, floa
 }
 
 // a2 standalone.
-__global__ __launch_bounds__(256) void k_var(float *__restrict__ v, const float *__restrict__ gbar,
+template <int GT>
+__global__ __launch_bounds__(256) void k_var(float *__restrict__ v, const void *__restrict__ gbar,
                                              int64_t n4, Scalars s)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n4) return;
-    f4v vv = ldnt(v, i), gb = ldnt(gbar, i);
+    f4v vv = ldnt(v, i), gb = ldg4<GT>(gbar, i);
 #pragma unroll
     for (int c = 0; c < 4; ++c) vv[c] = var_elem(vv[c], gb[c], s);
     stnt(v, i, vv);
@@ -271,10 +313,12 @@ __device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, boo
 // buffer lines when g != nullptr)
 // ---------------------------------------------------------------------------
 
-// UZ (with FUSED only): u is +0 everywhere and is not read.
-template <int L, int V, bool FUSED, bool UZ>
+// UZ (with FUSED only): u is +0 everywhere and is not read.  GT: element
+// type of g when FUSED, else of u (binary32 u, or the gradient itself under
+// Algorithm 4).
+template <int L, int V, bool FUSED, bool UZ, int GT>
 __global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
-    const float *__restrict__ g, const float *__restrict__ m, const float *__restrict__ u,
+    const void *__restrict__ g, const float *__restrict__ m, const void *__restrict__ u,
     float *__restrict__ err, Chunks ch, int64_t nchunks, uint32_t *__restrict__ packed32,
     float *__restrict__ scales, Scalars s)
 {
@@ -292,10 +336,11 @@ __global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
         a[k] = f4v{0.f, 0.f, 0.f, 0.f};
         if (e < len) {
             const int64_t i4 = (e0 + e) >> 2;
-            f4v uu = UZ ? f4v{0.f, 0.f, 0.f, 0.f} : ldnt(u, i4);
+            f4v uu = UZ ? f4v{0.f, 0.f, 0.f, 0.f}
+                        : (FUSED ? ldnt(static_cast<const float *>(u), i4) : ldg4<GT>(u, i4));
             const f4v dd = ldnt(err, i4);
             if (FUSED) {
-                const f4v gg = ldnt(g, i4), mm = ldnt(m, i4);
+                const f4v gg = ldg4<GT>(g, i4), mm = ldnt(m, i4);
 #pragma unroll
                 for (int q = 0; q < 4; ++q) uu[q] = uu[q] + s.gamma * (s.b1 * mm[q] + s.c1 * gg[q]);
             }
@@ -696,14 +741,14 @@ __device__ __forceinline__ bool chunk_slot(Chunks ch, int64_t nchunks, int bpc, 
     return c < nchunks && e < ch.len[c];
 }
 
-template <bool VAR, bool DEFER>
+template <bool VAR, bool DEFER, int GT>
 __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_packed32,
                                                const float *__restrict__ srv_scales, Chunks ch,
                                                int64_t nchunks, int bpc, int lb,
                                                float *__restrict__ m, float *__restrict__ x,
                                                float *__restrict__ v, float *__restrict__ u,
                                                float *__restrict__ anchor,
-                                               const float *__restrict__ gbar, float gsum,
+                                               const void *__restrict__ gbar, float gsum,
                                                Scalars s)
 {
     int64_t c;
@@ -714,7 +759,7 @@ __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_
     const uint32_t bits = srv_packed32[2 * ch.word[c] + (e >> 5)] >> (e & 31);
     const f4v vv = ldnt(v, i4), an = ldnt(anchor, i4);
     f4v gb;
-    if (VAR) gb = ldnt(gbar, i4);
+    if (VAR) gb = ldg4<GT>(gbar, i4);
     f4v mm, xx, nv;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -751,13 +796,14 @@ __device__ __forceinline__ void fv_elem(float gb, float &x, float &m, float &v, 
 }
 
 // t in T_v: gbar is the full-precision average.  One float4 per thread.
-__global__ __launch_bounds__(256) void k_fv_full(const float *__restrict__ gbar,
+template <int GT>
+__global__ __launch_bounds__(256) void k_fv_full(const void *__restrict__ gbar,
                                                  float *__restrict__ x, float *__restrict__ m,
                                                  float *__restrict__ v, int64_t n4, Scalars s)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n4) return;
-    const f4v gb = ldnt(gbar, i);
+    const f4v gb = ldg4<GT>(gbar, i);
     f4v xx = ldnt(x, i), mm = ldnt(m, i), vv = ldnt(v, i);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -920,22 +966,29 @@ static inline unsigned chunk_block() { return L > 256 ? L : 256; }
 template <int L>
 static inline int64_t chunks_per_block() { return L >= 256 ? 1 : 256 / L; }
 
-hipError_t launch_local(bool var, bool uz, const float *g, float *m, const float *x_src, float *x,
-                        float *v, float *u, const float *gbar, int64_t n, const Scalars &s,
+hipError_t launch_local(bool var, bool uz, const void *g, float *m, const float *x_src, float *x,
+                        float *v, float *u, const void *gbar, int64_t n, const Scalars &s, int gt,
                         hipStream_t st)
 {
     const int64_t n4 = n / 4;
     if (n4 == 0) return hipSuccess;
     const dim3 grid(grid_for(n4, 256)), block(256);
-    if (var && uz)
-        hipLaunchKernelGGL((k_local<true, true>), grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s);
-    else if (var)
-        hipLaunchKernelGGL((k_local<true, false>), grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s);
-    else if (uz)
-        hipLaunchKernelGGL((k_local<false, true>), grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s);
-    else
-        hipLaunchKernelGGL((k_local<false, false>), grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s);
-    return hipGetLastError();
+    return with_grad_type(gt, [&](auto T) {
+        constexpr int GT = decltype(T)::value;
+        if (var && uz)
+            hipLaunchKernelGGL((k_local<true, true, GT>), grid, block, 0, st, g, m, x_src, x, v,
+                               u, gbar, n4, s);
+        else if (var)
+            hipLaunchKernelGGL((k_local<true, false, GT>), grid, block, 0, st, g, m, x_src, x, v,
+                               u, gbar, n4, s);
+        else if (uz)
+            hipLaunchKernelGGL((k_local<false, true, GT>), grid, block, 0, st, g, m, x_src, x, v,
+                               u, gbar, n4, s);
+        else
+            hipLaunchKernelGGL((k_local<false, false, GT>), grid, block, 0, st, g, m, x_src, x,
+                               v, u, gbar, n4, s);
+        return hipGetLastError();
+    });
 }
 
 hipError_t launch_zero(float *dst, int64_t n, hipStream_t st)
@@ -946,34 +999,47 @@ hipError_t launch_zero(float *dst, int64_t n, hipStream_t st)
     return hipGetLastError();
 }
 
-hipError_t launch_var(float *v, const float *gbar, int64_t n, const Scalars &s, hipStream_t st)
+hipError_t launch_var(float *v, const void *gbar, int64_t n, const Scalars &s, int gt,
+                      hipStream_t st)
 {
     const int64_t n4 = n / 4;
     if (n4 == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_var, dim3(grid_for(n4, 256)), dim3(256), 0, st, v, gbar, n4, s);
-    return hipGetLastError();
+    return with_grad_type(gt, [&](auto T) {
+        constexpr int GT = decltype(T)::value;
+        hipLaunchKernelGGL((k_var<GT>), dim3(grid_for(n4, 256)), dim3(256), 0, st, v, gbar, n4,
+                           s);
+        return hipGetLastError();
+    });
 }
 
-hipError_t launch_sync1(Geometry geo, bool fused, bool uz, const float *g, const float *m,
-                        const float *u, float *err, const Chunks &ch, int64_t nchunks,
-                        uint64_t *packed, float *scales, const Scalars &s, hipStream_t st)
+hipError_t launch_sync1(Geometry geo, bool fused, bool uz, const void *g, const float *m,
+                        const void *u, float *err, const Chunks &ch, int64_t nchunks,
+                        uint64_t *packed, float *scales, const Scalars &s, int gt, int ut,
+                        hipStream_t st)
 {
     if (nchunks == 0) return hipSuccess;
     if (uz && !fused) return hipErrorInvalidValue;
-    return with_geometry(geo, [&](auto Lc, auto Vc) {
-        constexpr int L = decltype(Lc)::value, V = decltype(Vc)::value;
-        const unsigned grid = grid_for(nchunks, chunks_per_block<L>());
-        uint32_t *p32 = reinterpret_cast<uint32_t *>(packed);
-        if (uz)
-            hipLaunchKernelGGL((k_sync1<L, V, true, true>), dim3(grid), dim3(chunk_block<L>()), 0,
-                               st, g, m, u, err, ch, nchunks, p32, scales, s);
-        else if (fused)
-            hipLaunchKernelGGL((k_sync1<L, V, true, false>), dim3(grid), dim3(chunk_block<L>()),
-                               0, st, g, m, u, err, ch, nchunks, p32, scales, s);
-        else
-            hipLaunchKernelGGL((k_sync1<L, V, false, false>), dim3(grid), dim3(chunk_block<L>()),
-                               0, st, g, m, u, err, ch, nchunks, p32, scales, s);
-        return hipGetLastError();
+    if (fused && ut != GT_F32) return hipErrorInvalidValue;
+    return with_grad_type(fused ? gt : ut, [&](auto T) {
+        constexpr int GT = decltype(T)::value;
+        return with_geometry(geo, [&](auto Lc, auto Vc) {
+            constexpr int L = decltype(Lc)::value, V = decltype(Vc)::value;
+            const unsigned grid = grid_for(nchunks, chunks_per_block<L>());
+            uint32_t *p32 = reinterpret_cast<uint32_t *>(packed);
+            if (uz)
+                hipLaunchKernelGGL((k_sync1<L, V, true, true, GT>), dim3(grid),
+                                   dim3(chunk_block<L>()), 0, st, g, m, u, err, ch, nchunks, p32,
+                                   scales, s);
+            else if (fused)
+                hipLaunchKernelGGL((k_sync1<L, V, true, false, GT>), dim3(grid),
+                                   dim3(chunk_block<L>()), 0, st, g, m, u, err, ch, nchunks, p32,
+                                   scales, s);
+            else
+                hipLaunchKernelGGL((k_sync1<L, V, false, false, GT>), dim3(grid),
+                                   dim3(chunk_block<L>()), 0, st, g, m, u, err, ch, nchunks, p32,
+                                   scales, s);
+            return hipGetLastError();
+        });
     });
 }
 
@@ -1075,14 +1141,17 @@ static int64_t chunk_slots(int chunk, int64_t nchunks, int &bpc, int &lb)
     return (nchunks + (256 / lb) - 1) / (256 / lb);
 }
 
-hipError_t launch_fv_full(const float *gbar, float *x, float *m, float *v, int64_t n,
-                          const Scalars &s, hipStream_t st)
+hipError_t launch_fv_full(const void *gbar, float *x, float *m, float *v, int64_t n,
+                          const Scalars &s, int gt, hipStream_t st)
 {
     const int64_t n4 = n / 4;
     if (n4 == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_fv_full, dim3(grid_for(n4, 256)), dim3(256), 0, st, gbar, x, m, v, n4,
-                       s);
-    return hipGetLastError();
+    return with_grad_type(gt, [&](auto T) {
+        constexpr int GT = decltype(T)::value;
+        hipLaunchKernelGGL((k_fv_full<GT>), dim3(grid_for(n4, 256)), dim3(256), 0, st, gbar, x, m,
+                           v, n4, s);
+        return hipGetLastError();
+    });
 }
 
 hipError_t launch_fv_apply(const uint64_t *srv_packed, const float *srv_scales, const Chunks &ch,
@@ -1100,8 +1169,8 @@ hipError_t launch_fv_apply(const uint64_t *srv_packed, const float *srv_scales, 
 
 hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
-                        float *x, float *v, float *u, float *anchor, const float *gbar,
-                        float gsum, const Scalars &s, int chunk, hipStream_t st)
+                        float *x, float *v, float *u, float *anchor, const void *gbar,
+                        float gsum, const Scalars &s, int gt, int chunk, hipStream_t st)
 {
     (void)geo;
     if (nchunks == 0) return hipSuccess;
@@ -1109,19 +1178,22 @@ hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_
     const int64_t grid = chunk_slots(chunk, nchunks, bpc, lb);
     const uint32_t *p32 = reinterpret_cast<const uint32_t *>(srv_packed);
     const dim3 g3((unsigned)grid), b3(256);
-    if (var && defer)
-        hipLaunchKernelGGL((k_recon<true, true>), g3, b3, 0, st, p32, srv_scales, ch, nchunks, bpc,
-                           lb, m, x, v, u, anchor, gbar, gsum, s);
-    else if (var)
-        hipLaunchKernelGGL((k_recon<true, false>), g3, b3, 0, st, p32, srv_scales, ch, nchunks,
-                           bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
-    else if (defer)
-        hipLaunchKernelGGL((k_recon<false, true>), g3, b3, 0, st, p32, srv_scales, ch, nchunks,
-                           bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
-    else
-        hipLaunchKernelGGL((k_recon<false, false>), g3, b3, 0, st, p32, srv_scales, ch, nchunks,
-                           bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
-    return hipGetLastError();
+    return with_grad_type(gt, [&](auto T) {
+        constexpr int GT = decltype(T)::value;
+        if (var && defer)
+            hipLaunchKernelGGL((k_recon<true, true, GT>), g3, b3, 0, st, p32, srv_scales, ch,
+                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+        else if (var)
+            hipLaunchKernelGGL((k_recon<true, false, GT>), g3, b3, 0, st, p32, srv_scales, ch,
+                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+        else if (defer)
+            hipLaunchKernelGGL((k_recon<false, true, GT>), g3, b3, 0, st, p32, srv_scales, ch,
+                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+        else
+            hipLaunchKernelGGL((k_recon<false, false, GT>), g3, b3, 0, st, p32, srv_scales, ch,
+                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+        return hipGetLastError();
+    });
 }
 
 template <int R>

@@ -14,6 +14,20 @@ import synth
 from synth import configs as C
 
 
+def round_to(values, grad_dtype):
+    """Binary32 values rounded to nearest-even in the 16-bit gradient type
+    (and back, exactly): what the GPU side receives, converted on the device
+    by torch, and what the oracle is fed."""
+    a = np.ascontiguousarray(values, dtype=np.float32)
+    if grad_dtype == "f32":
+        return a
+    if grad_dtype == "f16":
+        return a.astype(np.float16).astype(np.float32)
+    b = a.view(np.uint32).astype(np.uint64)
+    r = ((b + 0x7FFF + ((b >> 16) & 1)) >> 16) << 16
+    return (r & 0xFFFFFFFF).astype(np.uint32).view(np.float32)
+
+
 def steps_kind(wl, t):
     """(sync, var): Algorithm 1 -- t in T_u, t in T_v.  Algorithm 4 -- a
     compressed step is t outside T_v, a full-precision step t in T_v."""
@@ -66,8 +80,9 @@ def sample_chunks(lay, seg_off, budget_elems, stride_chunks=None):
 # ---------------------------------------------------------------------------
 
 class OracleRun:
-    def __init__(self, wl, chunk_ids=None, literal=False):
+    def __init__(self, wl, chunk_ids=None, literal=False, grad_dtype="f32"):
         self.wl = wl
+        self.grad_dtype = grad_dtype
         self.full = orc.Layout.from_segments(wl.seg_off, wl.chunk)
         if chunk_ids is None:
             chunk_ids = np.arange(self.full.nchunks, dtype=np.int64)
@@ -95,13 +110,13 @@ class OracleRun:
 
     def grad(self, t):
         wl = self.wl
-        return self.gather_normal(C.STREAM_G, t, wl.sigma_g, wl.outlier_per_mille,
-                                  wl.outlier_factor)
+        return round_to(self.gather_normal(C.STREAM_G, t, wl.sigma_g, wl.outlier_per_mille,
+                                           wl.outlier_factor), self.grad_dtype)
 
     def gbar(self, t):
         wl = self.wl
-        return self.gather_normal(C.STREAM_GBAR, t, wl.sigma_g, wl.outlier_per_mille,
-                                  wl.outlier_factor)
+        return round_to(self.gather_normal(C.STREAM_GBAR, t, wl.sigma_g, wl.outlier_per_mille,
+                                           wl.outlier_factor), self.grad_dtype)
 
     def peers(self, t):
         wl = self.wl
@@ -144,10 +159,13 @@ class GpuRun:
     STATE = ("x", "m", "v", "u", "err", "srv_err", "anchor")
     FV_STATE = ("x", "m", "v", "err", "srv_err")
 
-    def __init__(self, wl, device="cuda", fused=True, srv_range=(0, -1), defer=False):
+    def __init__(self, wl, device="cuda", fused=True, srv_range=(0, -1), defer=False,
+                 grad_dtype="f32"):
         import torch
         import paper_2202_06009_amd as zo
         self.torch, self.zo, self.wl, self.fused = torch, zo, wl, fused
+        self.grad_dtype = grad_dtype
+        self.gdt = {"f32": None, "f16": torch.float16, "bf16": torch.bfloat16}[grad_dtype]
         self.fv = wl.algorithm == "frozen-variance"
         self.keys = self.FV_STATE if self.fv else self.STATE
         n = wl.n
@@ -169,7 +187,7 @@ class GpuRun:
                              chunk=wl.chunk, seg_off=wl.seg_off, tv=wl.tv, tu=wl.tu,
                              state=self.state, srv_chunk_begin=srv_range[0],
                              srv_chunk_end=srv_range[1], defer_sync_writes=defer,
-                             algorithm=wl.algorithm)
+                             algorithm=wl.algorithm, grad_dtype=grad_dtype)
 
     def fill_inputs(self, t):
         wl = self.wl
@@ -181,6 +199,10 @@ class GpuRun:
             if var:
                 synth.normal_dev(self.gb[:n], 0, synth.key(0, C.STREAM_GBAR, t),
                                  C.ksigma(wl.sigma_g), wl.outlier_per_mille, wl.outlier_factor)
+        if self.gdt is not None:
+            self.g_in, self.gb_in = self.g.to(self.gdt), self.gb.to(self.gdt)
+        else:
+            self.g_in, self.gb_in = self.g, self.gb
         if sync and self.nwords:
             base = wl.peer_scale_base(t)
             for w in range(1, wl.world):
@@ -191,8 +213,8 @@ class GpuRun:
         wl = self.wl
         sync, var = steps_kind(wl, t)
         self.fill_inputs(t)
-        g = self.g
-        gb = self.gb if var else None
+        g = self.g_in
+        gb = self.gb_in if var else None
         o = self.opt
         gam = wl.gamma(t)
         if self.fv:
@@ -290,12 +312,13 @@ class Comparator:
 
 
 def run_parity(wl, steps=None, chunk_ids=None, fused=True, log=None, defer=False,
-               materialize_at=()):
+               materialize_at=(), grad_dtype="f32"):
     """Run both sides for `steps` steps; return per-step mismatch dicts.
     defer: deferred sync writes (the logical state is compared);
-    materialize_at: steps after which the deferred writes are forced out."""
-    grun = GpuRun(wl, fused=fused, defer=defer)
-    orun = OracleRun(wl, chunk_ids)
+    materialize_at: steps after which the deferred writes are forced out;
+    grad_dtype: element type of the gradients handed to the library."""
+    grun = GpuRun(wl, fused=fused, defer=defer, grad_dtype=grad_dtype)
+    orun = OracleRun(wl, chunk_ids, grad_dtype=grad_dtype)
     cmp_ = Comparator(grun, orun)
     report = []
     try:
