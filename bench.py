@@ -41,14 +41,20 @@ COPY_BYTES = 4 << 30          # size of the calibration copies
 # The second template argument of k_local / k_recon is the deferred variant
 # (the very first local step of a run has no sync before it and is skipped).
 def kernel_keys(mode):
+    """Kernel-name prefixes of the timed kernels for a mode ("deferred",
+    "eager" or "frozen-variance", with "/f16" or "/bf16" for 16-bit
+    gradients); the last template argument of the gradient-reading kernels
+    is the gradient type (0 binary32, 1 binary16, 2 bfloat16)."""
     copies = {"zo::k_copy<true>": ("copy_nt", None), "zo::k_copy<false>": ("copy_plain", None)}
-    if mode == "frozen-variance":
-        return {"zo::k_fv_full": ("fv_full", "nt"), "zo::k_sync1<": ("sync1", "nt"),
+    base, _, dt = mode.partition("/")
+    gt = {"": 0, "f16": 1, "bf16": 2}[dt]
+    if base == "frozen-variance":
+        return {f"zo::k_fv_full<{gt}>": ("fv_full", "nt"), "zo::k_sync1<": ("sync1", "nt"),
                 "zo::k_srv_lut<": ("srv", "plain"), "zo::k_fv_apply": ("fv_apply", "nt")} | copies
-    dv = "true" if mode == "deferred" else "false"
-    return {f"zo::k_local<true, {dv}>": ("local+var", "nt"), "zo::k_sync1<": ("sync1", "nt"),
-            "zo::k_srv_lut<": ("srv", "plain"), f"zo::k_recon<true, {dv}>": ("recon+var", "nt")
-            } | copies
+    dv = "true" if base == "deferred" else "false"
+    return {f"zo::k_local<true, {dv}, {gt}>": ("local+var", "nt"), "zo::k_sync1<": ("sync1", "nt"),
+            "zo::k_srv_lut<": ("srv", "plain"),
+            f"zo::k_recon<true, {dv}, {gt}>": ("recon+var", "nt")} | copies
 
 
 def source_hash():
