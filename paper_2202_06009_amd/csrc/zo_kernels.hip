@@ -614,6 +614,12 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
     const int64_t off = 2 * wd;
     constexpr bool kUni = LD >= 64;  // a wave never spans two chunks
     uint32_t ring[kSrvPrefetch + 1][8];
+    // the first groups' packed words are in flight while the tables are built
+    if (has_dw) {
+#pragma unroll
+        for (int g = 0; g < kSrvPrefetch && g < G; ++g)
+            load_group<kUni>(ring[g], packed32, off, ws, g, W, lc);
+    }
 
     // stage the scales of the workgroup's chunks, then build the tables
     for (int i = threadIdx.x; i < CPW * W; i += blockDim.x) {
@@ -637,14 +643,24 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
         }
         half[i] = t;
     }
-    {
-        const uint32_t f = inexact_flag<LD>(sc + q * W, 1, W, lc);
-        if (active && lc == 0) flags[cr] = (uint8_t)f;
-    }
     __syncthreads();
-    for (int i = threadIdx.x; i < CPW * G * 256; i += blockDim.x) {
-        const int qg = i >> 8, b = i & 255;  // qg = chunk * G + group
-        tab[i] = half[32 * qg + (b & 15)] + half[32 * qg + 16 + (b >> 4)];
+    {
+        // CPW * G * 256 entries over LD * CPW threads, kPer each (both powers
+        // of two; a thread with no entry of its own repeats one): every read
+        // is issued before the first add
+        constexpr int kTotal = CPW * G * 256, kThreads = LD * CPW;
+        constexpr int kPer = kTotal >= kThreads ? kTotal / kThreads : 1;
+        double lo[kPer], hi[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int i = ((int)threadIdx.x + k * kThreads) % kTotal;
+            const int qg = i >> 8, b = i & 255;  // qg = chunk * G + group
+            lo[k] = half[32 * qg + (b & 15)];
+            hi[k] = half[32 * qg + 16 + (b >> 4)];
+        }
+#pragma unroll
+        for (int k = 0; k < kPer; ++k)
+            tab[((int)threadIdx.x + k * kThreads) % kTotal] = lo[k] + hi[k];
     }
     __syncthreads();
     const char *mytab = reinterpret_cast<const char *>(tab) + (size_t)q * G * 2048;
@@ -667,9 +683,6 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
     for (int i = 0; i < 32; ++i) acc[i] = 0.0;
     if (has_dw) {
 #pragma unroll
-        for (int g = 0; g < kSrvPrefetch && g < G; ++g)
-            load_group<kUni>(ring[g], packed32, off, ws, g, W, lc);
-#pragma unroll
         for (int g = 0; g < G; ++g) {
             if (g + kSrvPrefetch < G)
                 load_group<kUni>(ring[(g + kSrvPrefetch) % (kSrvPrefetch + 1)], packed32, off,
@@ -685,6 +698,10 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
         }
     } else {
         load_serr();
+    }
+    {
+        const uint32_t f = inexact_flag<LD>(sc + q * W, 1, W, lc);
+        if (active && lc == 0) flags[cr] = (uint8_t)f;
     }
 
     // averages -> LDS, then back in the coalesced layout of the compress step
