@@ -563,10 +563,6 @@ __device__ __forceinline__ void lookup8(double (&acc)[32], const uint32_t (&x)[8
                  : "memory");
 }
 
-// LD lanes per chunk (one packed dword each), G groups of 8 workers (a
-// compile-time count; groups past the last worker hold zero tables).  The tables of chunk q of the workgroup start at byte q*G*2048 of
-// `tab`; with one chunk per workgroup the offset of every lookup is an
-// immediate.
 // Float4 slot of the transpose buffer that holds float4 t of a chunk (t = e/4).
 // Lane j writes the slots 8j..8j+7 of its dword; lanes then read slots in
 // coalesced order.  XOR-ing the slot's low three bits with bits 1..3 of j makes
@@ -577,6 +573,11 @@ __device__ __forceinline__ int xpose_slot(int t)
     return 8 * (t >> 3) + ((t & 7) ^ ((t >> 4) & 7));
 }
 
+// LD lanes per chunk (one packed dword each), G groups of 8 workers (a
+// compile-time count; groups past the last worker hold zero tables), CPW
+// chunks per workgroup.  The tables of chunk q of the workgroup start at byte
+// q*G*2048 of `tab`; with one chunk per workgroup the offset of every lookup is
+// an immediate.
 template <int LD, int G>
 __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
     const uint32_t *__restrict__ packed32, const float *__restrict__ scales, int W,

@@ -234,3 +234,12 @@ def test_workload_sampled(torch_cuda, name):
          f"{int((lay.clen[ids] != wl.chunk).sum())} ragged")
     report, inexact = harness.run_parity(wl, chunk_ids=ids, log=_log)
     _assert_clean(report, inexact)
+
+
+def test_largest_world(torch_cuda):
+    """W = 65536, the largest worker count the library takes (the plain server:
+    its tables would not fit in LDS), on a small ragged shard."""
+    import harness
+    wl = _small("w65536", [2048, 100], 1024, 65536, steps=3, tu=[1, 2], tv=[0])
+    report, inexact = harness.run_parity(wl, log=_log)
+    _assert_clean(report, inexact)
