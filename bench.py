@@ -9,9 +9,10 @@ optimizer steps that together run every kernel of the path once:
                                        K_srv, W = 128      (zo_unpack_average)
                                        K_recon+var         (zo_sync_update)
 The reconstruction defers its x and u writes (the new model stays in the
-anchor buffer, u is an implicit zero that the next local step does not read;
-same values, 12 bytes per parameter less per bench step); --eager-sync-writes
-times the eager variant.
+anchor buffer, u is an implicit zero; the next local step writes x but leaves
+u = +0 + gamma m implicit, which the compress forms from the m it reads; same
+values, 20 bytes per parameter less per bench step); --eager-sync-writes times
+the eager variant.
 Inputs (gradient, averaged gradient, peers' packed signs and scales) are
 generated once on the device before timing and stay resident in HBM.
 `value` is optimizer-step parameter updates per second (2 d per bench step).
@@ -52,7 +53,10 @@ def kernel_keys(mode):
         return {f"zo::k_fv_full<{gt}>": ("fv_full", "nt"), "zo::k_sync1<": ("sync1", "nt"),
                 "zo::k_srv_lut<": ("srv", "plain"), "zo::k_fv_apply": ("fv_apply", "nt")} | copies
     dv = "true" if base == "deferred" else "false"
-    return {f"zo::k_local<true, {dv}, {gt}>": ("local+var", "nt"), "zo::k_sync1<": ("sync1", "nt"),
+    # k_local<VAR, UIN, WU, GT>: deferred, the local step after a sync has
+    # UIN = 1 (u = +0) and WU = false; eager UIN = 0, WU = true
+    lv = f"true, 1, false, {gt}" if base == "deferred" else f"true, 0, true, {gt}"
+    return {f"zo::k_local<{lv}>": ("local+var", "nt"), "zo::k_sync1<": ("sync1", "nt"),
             "zo::k_srv_lut<": ("srv", "plain"),
             f"zo::k_recon<true, {dv}, {gt}>": ("recon+var", "nt")} | copies
 
@@ -138,15 +142,16 @@ def algorithmic_bytes(d, nchunks, nwords, W, deferred=True, gbytes=4):
     """Bytes each kernel must move per launch: every state read once and
     written once, packed words and per-chunk scales included (gbytes: bytes
     per gradient element of g and gbar).  With deferred sync writes the local
-    step after a sync reads x from the anchor and does not read u, and the
-    reconstruction writes neither x nor u."""
+    step after a sync reads x from the anchor and neither reads nor writes u
+    (u = +0 + gamma m there), the compress that follows forms u from the m it
+    reads, and the reconstruction writes neither x nor u."""
     pk = 8 * nwords
     sc = 4 * nchunks
     return {
-        # reads g, m, x, v, u (eager only), gbar; writes m, x, u, v
-        "local+var": ((28 if deferred else 32) + 2 * gbytes) * d,
-        # reads g, m, u, err; writes err, own packed words, own scales
-        "sync1": (16 + gbytes) * d + pk + sc,
+        # reads g, m, x, v, gbar, u (eager only); writes m, x, v, u (eager only)
+        "local+var": ((24 if deferred else 32) + 2 * gbytes) * d,
+        # reads g, m, err, u (eager only); writes err, own packed words, own scales
+        "sync1": ((12 if deferred else 16) + gbytes) * d + pk + sc,
         # reads W packed buffers + W scale rows + server error;
         # writes server error, server packed words, server scales
         "srv": W * (pk + sc) + 8 * d + pk + sc,
@@ -169,9 +174,9 @@ def stream_mix_ceilings(zo, torch, state, g, gb, d, mode):
         "fv_apply": ([S["x"], S["m"], S["v"]], [S["u"], S["anchor"]]),
     } if mode == "frozen-variance" else {
         "local+var": ([g, gb, S["m"], S["anchor"], S["v"]] + ([] if deferred else [S["u"]]),
-                      [S["x"], S["u"], S["err"], S["srv_err"]] if deferred else
+                      [S["x"], S["err"], S["srv_err"]] if deferred else
                       [S["x"], S["err"], S["srv_err"], S["anchor"]]),
-        "sync1": ([g, S["m"], S["u"], S["err"]], [S["x"]]),
+        "sync1": ([g, S["m"], S["err"]] + ([] if deferred else [S["u"]]), [S["x"]]),
         "recon+var": ([S["v"], S["anchor"], gb],
                       [S["m"], S["x"], S["u"]] if deferred else
                       [S["m"], S["x"], S["u"], S["err"]]),

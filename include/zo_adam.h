@@ -96,12 +96,17 @@ typedef struct zo_adam zo_adam;   /* opaque handle */
  *                  0: zo_sync_update writes x, anchor and u = 0 (x and u are
  *                  always current in their buffers).  Nonzero: it writes only
  *                  m and the anchor (8 bytes per parameter less); the new
- *                  model is then held in `anchor` and u is +0 by definition,
- *                  and the next zo_local_step reads the model from the anchor
- *                  and does not read u (4 bytes less), writing both back.
- *                  Until then zo_state_location says where the model is, and
- *                  zo_materialize writes x and u out.  The arithmetic, and so
- *                  every value, is the same in both modes.
+ *                  model is then held in `anchor` and u is +0 by definition.
+ *                  The next zo_local_step reads the model from the anchor and
+ *                  writes x, and neither reads nor writes u (8 bytes less):
+ *                  u is then +0 + gamma_t m_{t+1} in binary32, the one
+ *                  product it added, so the next call that needs u (a local
+ *                  step, which writes it, or a fused compress) forms it from
+ *                  the m it reads anyway (4 bytes less).  A local step at a
+ *                  sync step (the unfused path) always writes u.
+ *                  zo_state_location says where x and u are; zo_materialize
+ *                  writes them out.  The arithmetic, and so every value, is
+ *                  the same in both modes.
  *   algorithm      ZO_ALG_ZERO_ONE_ADAM (default 0) or ZO_ALG_FROZEN_VARIANCE.
  *                  The latter requires ntu = 0 and defer_sync_writes = 0; its
  *                  steps are zo_fullprec_step at t in T_v and, at every other
@@ -254,9 +259,9 @@ int zo_fullprec_step(zo_adam *h, int64_t t, float gamma, const void *gbar);
 int zo_variance_update(zo_adam *h, int64_t t, const void *gbar);
 
 /*
- * zo_materialize -- with defer_sync_writes, write out what the last
- * zo_sync_update left implicit: x <- anchor and u <- +0 (one copy and one fill
- * kernel on the handle's stream, only for what is pending).  Between steps
+ * zo_materialize -- with defer_sync_writes, write out what is implicit:
+ * x <- anchor, and u <- +0 or +0 + gamma m (one copy and one fill kernel on
+ * the handle's stream, only for what is pending).  Between steps
  * only (ZO_ESTATE otherwise); changes no value of the optimizer state.  The
  * next steps run as after an eager zo_sync_update.
  */
@@ -264,9 +269,11 @@ int zo_materialize(zo_adam *h);
 
 /* ---- queries (host only; never touch the device unless stated) ---------- */
 /* Where the current state is: *x_now = the device buffer that holds x
- * (st.x, or st.anchor after a deferred zo_sync_update); *u_is_zero = 1 when
- * u is +0 everywhere and st.u is stale, else 0.  Either pointer may be NULL. */
-int zo_state_location(const zo_adam *h, float **x_now, int32_t *u_is_zero);
+ * (st.x, or st.anchor after a deferred zo_sync_update); *u_mode = 0 when
+ * st.u holds u, 1 when u is +0 everywhere, 2 when u = +0 + (*u_gamma) * m
+ * elementwise in binary32 (st.u stale in modes 1 and 2; *u_gamma is 0 in modes
+ * 0 and 1).  Any pointer may be NULL. */
+int zo_state_location(const zo_adam *h, float **x_now, int32_t *u_mode, float *u_gamma);
 int64_t zo_num_chunks(const zo_adam *h);
 int64_t zo_packed_words(const zo_adam *h);
 /* Server range: first chunk, chunk count, first word, word count, first

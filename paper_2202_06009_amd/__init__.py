@@ -79,7 +79,8 @@ def lib():
             "zo_variance_update": ([vp, i64, vp], ci),
             "zo_materialize": ([vp], ci),
             "zo_fullprec_step": ([vp, i64, f32, vp], ci),
-            "zo_state_location": ([vp, ctypes.POINTER(vp), ctypes.POINTER(i32)], ci),
+            "zo_state_location": ([vp, ctypes.POINTER(vp), ctypes.POINTER(i32),
+                                   ctypes.POINTER(f32)], ci),
             "zo_num_chunks": ([vp], i64),
             "zo_packed_words": ([vp], i64),
             "zo_server_range": ([vp, pi64, pi64, pi64, pi64, pi64, pi64], ci),
@@ -226,14 +227,19 @@ def zo_materialize(h):
     _call(h, "zo_materialize")
 
 
+U_IN_BUFFER, U_ZERO, U_GAMMA_M = 0, 1, 2
+
+
 def zo_state_location(h):
-    """(device address of the buffer holding x, u_is_zero)."""
+    """(device address of the buffer holding x, u mode, u gamma): u is in its
+    buffer (U_IN_BUFFER), +0 (U_ZERO) or +0 + gamma * m (U_GAMMA_M)."""
     x = ctypes.c_void_p()
-    uz = ctypes.c_int32()
-    rc = lib().zo_state_location(h, ctypes.byref(x), ctypes.byref(uz))
+    mode = ctypes.c_int32()
+    gam = ctypes.c_float()
+    rc = lib().zo_state_location(h, ctypes.byref(x), ctypes.byref(mode), ctypes.byref(gam))
     if rc != ZO_OK:
         raise ZoError(rc, "zo_state_location")
-    return x.value, bool(uz.value)
+    return x.value, mode.value, gam.value
 
 
 def zo_adam_destroy(h):
@@ -329,11 +335,16 @@ class ZoAdam:
         deferred sync; u then reads as zeros)."""
         if self.cfg["algorithm"] != "zero-one":
             return self.state[name]
-        xp, uz = zo_state_location(self.h)
+        xp, mode, gam = zo_state_location(self.h)
         if name == "x" and xp == self.state["anchor"].data_ptr():
             return self.state["anchor"]
-        if name == "u" and uz:
+        if name == "u" and mode == U_ZERO:
             return self.state["u"].new_zeros(self.state["u"].shape)
+        if name == "u" and mode == U_GAMMA_M:
+            # the library's definition, binary32: +0 + gamma * m (view only)
+            import torch
+            g32 = torch.tensor(gam, dtype=torch.float32, device=self.state["m"].device)
+            return (self.state["m"] * g32) + 0.0
         return self.state[name]
 
     # queries

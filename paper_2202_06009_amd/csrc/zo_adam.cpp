@@ -73,9 +73,12 @@ struct zo_adam {
     float gamma_sum = 0.0f;
     int srv_algo = zo::SRV_AUTO;
     // Deferred sync writes: the reconstruction leaves the new model only in
-    // the anchor (x_in_anchor) and u = 0 implicit (u_zero) until the next
-    // local step writes them (or zo_materialize).
-    bool defer = false, x_in_anchor = false, u_zero = false;
+    // the anchor (x_in_anchor) and u = +0 implicit (u_in = U_ZERO); the first
+    // local step after it writes x but leaves u = +0 + gamma m implicit too
+    // (U_GM, gamma_u = its gamma), the next one writes u (or zo_materialize).
+    bool defer = false, x_in_anchor = false;
+    int u_in = zo::U_MEM;
+    float gamma_u = 0.0f;
     // Algorithm 4 instead of Algorithm 1; fv_gamma = gamma_t of the step whose
     // compressed average zo_sync_update applies.
     bool fv = false;
@@ -311,10 +314,20 @@ int zo_local_step(zo_adam *h, int64_t t, float gamma, const void *g, const void 
     zo::Scalars s = h->sc;
     s.gamma = gamma;
     const float *x_src = h->x_in_anchor ? h->st.anchor : h->st.x;
-    hipError_t e = zo::launch_local(gbar != nullptr, h->u_zero, g, h->st.m, x_src, h->st.x,
-                                    h->st.v, h->st.u, gbar, h->n, s, h->gt, h->stream);
+    // u stays implicit after the first local step since a deferred reset,
+    // unless a compress of u itself (the unfused sync) follows
+    const bool write_u = !(h->u_in == zo::U_ZERO && !tu);
+    s.gamma_u = h->gamma_u;
+    hipError_t e = zo::launch_local(gbar != nullptr, h->u_in, write_u, g, h->st.m, x_src,
+                                    h->st.x, h->st.v, h->st.u, gbar, h->n, s, h->gt, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
-    h->x_in_anchor = h->u_zero = false;
+    h->x_in_anchor = false;
+    if (write_u) {
+        h->u_in = zo::U_MEM;
+    } else {
+        h->u_in = zo::U_GM;
+        h->gamma_u = gamma;
+    }
     h->gamma_sum = h->gamma_sum + gamma;
     if (tu)
         h->phase = PH_LOCAL_SYNC;
@@ -338,7 +351,7 @@ int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const void *g, uint6
         if (bad_gamma(gamma)) return ZO_EINVAL;
         if (t != h->t || h->phase != PH_IDLE || h->in_tv(t)) return ZO_ESTATE;
         zo::Scalars s = h->sc;
-        hipError_t e = zo::launch_sync1(h->geo, false, false, nullptr, nullptr, g, h->st.err,
+        hipError_t e = zo::launch_sync1(h->geo, false, zo::U_MEM, nullptr, nullptr, g, h->st.err,
                                         h->ch, h->nchunks, packed0, scales0, s, zo::GT_F32,
                                         h->gt, h->stream);
         if (e != hipSuccess) return h->hip_fail(e);
@@ -356,11 +369,12 @@ int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const void *g, uint6
     }
     zo::Scalars s = h->sc;
     s.gamma = fused ? gamma : 0.0f;
-    // (after zo_local_step at this step u has been written, so u_zero is false
-    // on the unfused path)
-    hipError_t e = zo::launch_sync1(h->geo, fused, fused && h->u_zero, g, h->st.m, h->st.u,
-                                    h->st.err, h->ch, h->nchunks, packed0, scales0, s, h->gt,
-                                    zo::GT_F32, h->stream);
+    s.gamma_u = h->gamma_u;
+    // (after zo_local_step at this step u has been written: U_MEM on the
+    // unfused path)
+    hipError_t e = zo::launch_sync1(h->geo, fused, fused ? h->u_in : zo::U_MEM, g, h->st.m,
+                                    h->st.u, h->st.err, h->ch, h->nchunks, packed0, scales0, s,
+                                    h->gt, zo::GT_F32, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     if (fused) h->gamma_sum = h->gamma_sum + gamma;
     h->phase = PH_COMPRESSED;
@@ -412,7 +426,10 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
                                     h->st.anchor, gbar, h->gamma_sum, h->sc, h->gt, h->chunk,
                                     h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
-    if (h->defer) h->x_in_anchor = h->u_zero = true;
+    if (h->defer) {
+        h->x_in_anchor = true;
+        h->u_in = zo::U_ZERO;
+    }
     h->gamma_sum = 0.0f;
     if (tv && !gbar)
         h->phase = PH_VAR_PENDING;
@@ -448,11 +465,12 @@ int zo_variance_update(zo_adam *h, int64_t t, const void *gbar)
     return ZO_OK;
 }
 
-int zo_state_location(const zo_adam *h, float **x_now, int32_t *u_is_zero)
+int zo_state_location(const zo_adam *h, float **x_now, int32_t *u_mode, float *u_gamma)
 {
     if (!h) return ZO_EINVAL;
     if (x_now) *x_now = h->x_in_anchor ? h->st.anchor : h->st.x;
-    if (u_is_zero) *u_is_zero = h->u_zero ? 1 : 0;
+    if (u_mode) *u_mode = h->u_in;
+    if (u_gamma) *u_gamma = h->u_in == zo::U_GM ? h->gamma_u : 0.0f;
     return ZO_OK;
 }
 
@@ -465,11 +483,14 @@ int zo_materialize(zo_adam *h)
         if (e != hipSuccess) return h->hip_fail(e);
     }
     h->x_in_anchor = false;
-    if (h->u_zero) {
+    if (h->u_in == zo::U_ZERO) {
         hipError_t e = zo::launch_zero(h->st.u, h->n, h->stream);
         if (e != hipSuccess) return h->hip_fail(e);
+    } else if (h->u_in == zo::U_GM) {
+        hipError_t e = zo::launch_u_from_m(h->st.u, h->st.m, h->n, h->gamma_u, h->stream);
+        if (e != hipSuccess) return h->hip_fail(e);
     }
-    h->u_zero = false;
+    h->u_in = zo::U_MEM;
     return ZO_OK;
 }
 

@@ -10,7 +10,14 @@ namespace zo {
 // in binary32 on the host once, so every kernel uses the same constants.
 struct Scalars {
     float b1, c1, b2, c2, eps, gamma;
+    float gamma_u;  // U_GM: the buffer is +0 + gamma_u * m (see BufferIn)
 };
+
+// Where a kernel finds the buffer u.  U_MEM: in memory.  U_ZERO: +0 (reset by
+// the last synchronisation, not yet written).  U_GM: u = +0 + gamma_u * m with
+// m the momentum before this step (the only local step since the reset ran
+// with gamma_u and wrote m; binary32, so the product is the value it added).
+enum BufferIn { U_MEM = 0, U_ZERO = 1, U_GM = 2 };
 
 // Device chunk table: start element, length, first packed word.
 struct Chunks {
@@ -35,16 +42,20 @@ enum GradType { GT_F32 = 0, GT_F16 = 1, GT_BF16 = 2 };
 // Server-average algorithm.
 enum SrvAlgo { SRV_AUTO = 0, SRV_PLAIN = 1 };
 
-// uz: u is +0 and not read (a deferred reset); x_src may equal x.
-hipError_t launch_local(bool var, bool uz, const void *g, float *m, const float *x_src, float *x,
-                        float *v, float *u, const void *gbar, int64_t n, const Scalars &s, int gt,
-                        hipStream_t st);
+// u_in: where u is (BufferIn); write_u: false only with U_ZERO, leaving
+// u = gamma * m implicit; x_src may equal x.
+hipError_t launch_local(bool var, int u_in, bool write_u, const void *g, float *m,
+                        const float *x_src, float *x, float *v, float *u, const void *gbar,
+                        int64_t n, const Scalars &s, int gt, hipStream_t st);
+// u = +0 + gamma_u * m (writes out an implicit U_GM buffer).
+hipError_t launch_u_from_m(float *u, const float *m, int64_t n, float gamma_u, hipStream_t st);
 hipError_t launch_zero(float *dst, int64_t n, hipStream_t st);
 hipError_t launch_var(float *v, const void *gbar, int64_t n, const Scalars &s, int gt,
                       hipStream_t st);
-// gt: element type of g (fused); ut: of u, the compressed source when not
-// fused (binary32 u, or the gradient under Algorithm 4).
-hipError_t launch_sync1(Geometry geo, bool fused, bool uz, const void *g, const float *m,
+// u_in (fused only): where u is (BufferIn).  gt: element type of g (fused);
+// ut: of u, the compressed source when not fused (binary32 u, or the
+// gradient under Algorithm 4).
+hipError_t launch_sync1(Geometry geo, bool fused, int u_in, const void *g, const float *m,
                         const void *u, float *err, const Chunks &ch, int64_t nchunks,
                         uint64_t *packed, float *scales, const Scalars &s, int gt, int ut,
                         hipStream_t st);

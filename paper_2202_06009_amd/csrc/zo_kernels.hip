@@ -124,11 +124,27 @@ __device__ __forceinline__ float var_elem(float v, float gb, const Scalars &s)
 // a1 (+a2): local step, one float4 per thread
 // ---------------------------------------------------------------------------
 
+// The buffer before this step, per BufferIn (m_old: the momentum read).
+template <int UIN>
+__device__ __forceinline__ f4v buffer_in(const float *u, int64_t i4, f4v m_old, const Scalars &s)
+{
+    if constexpr (UIN == U_MEM) {
+        return ldnt(u, i4);
+    } else if constexpr (UIN == U_ZERO) {
+        return f4v{0.f, 0.f, 0.f, 0.f};
+    } else {
+        f4v r;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) r[q] = 0.0f + s.gamma_u * m_old[q];
+        return r;
+    }
+}
+
 // The model is read from x_src (x itself, or the anchor when the last
-// synchronisation left the model there) and written to x.  UZ: u is +0
-// everywhere (reset by the last synchronisation and not yet written), so it
-// is not read.
-template <bool VAR, bool UZ, int GT>
+// synchronisation left the model there) and written to x.  UIN: where u is
+// (BufferIn).  WU: write u (false only with U_ZERO: the new u = +0 + gamma m'
+// is then left implicit, U_GM for the next call).
+template <bool VAR, int UIN, bool WU, int GT>
 __global__ __launch_bounds__(256) void k_local(const void *__restrict__ g, float *__restrict__ m,
                                                const float *x_src, float *x,
                                                float *__restrict__ v, float *__restrict__ u,
@@ -138,7 +154,7 @@ __global__ __launch_bounds__(256) void k_local(const void *__restrict__ g, float
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n4) return;
     f4v gg = ldg4<GT>(g, i), mm = ldnt(m, i), xx = ldnt(x_src, i), vv = ldnt(v, i);
-    f4v uu = UZ ? f4v{0.f, 0.f, 0.f, 0.f} : ldnt(u, i);
+    f4v uu = buffer_in<UIN>(u, i, mm, s);
     f4v gb;
     if (VAR) gb = ldg4<GT>(gbar, i);
 #pragma unroll
@@ -151,7 +167,7 @@ __global__ __launch_bounds__(256) void k_local(const void *__restrict__ g, float
     }
     stnt(m, i, mm);
     stnt(x, i, xx);
-    stnt(u, i, uu);
+    if (WU) stnt(u, i, uu);
     if (VAR) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) vv[c] = var_elem(vv[c], gb[c], s);
@@ -313,10 +329,10 @@ __device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, boo
 // buffer lines when g != nullptr)
 // ---------------------------------------------------------------------------
 
-// UZ (with FUSED only): u is +0 everywhere and is not read.  GT: element
+// UIN (with FUSED only; U_MEM otherwise): where u is (BufferIn).  GT: element
 // type of g when FUSED, else of u (binary32 u, or the gradient itself under
 // Algorithm 4).
-template <int L, int V, bool FUSED, bool UZ, int GT>
+template <int L, int V, bool FUSED, int UIN, int GT>
 __global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
     const void *__restrict__ g, const float *__restrict__ m, const void *__restrict__ u,
     float *__restrict__ err, Chunks ch, int64_t nchunks, uint32_t *__restrict__ packed32,
@@ -336,13 +352,15 @@ __global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
         a[k] = f4v{0.f, 0.f, 0.f, 0.f};
         if (e < len) {
             const int64_t i4 = (e0 + e) >> 2;
-            f4v uu = UZ ? f4v{0.f, 0.f, 0.f, 0.f}
-                        : (FUSED ? ldnt(static_cast<const float *>(u), i4) : ldg4<GT>(u, i4));
             const f4v dd = ldnt(err, i4);
+            f4v uu;
             if (FUSED) {
                 const f4v gg = ldg4<GT>(g, i4), mm = ldnt(m, i4);
+                uu = buffer_in<UIN>(static_cast<const float *>(u), i4, mm, s);
 #pragma unroll
                 for (int q = 0; q < 4; ++q) uu[q] = uu[q] + s.gamma * (s.b1 * mm[q] + s.c1 * gg[q]);
+            } else {
+                uu = ldg4<GT>(u, i4);
             }
 #pragma unroll
             for (int q = 0; q < 4; ++q) a[k][q] = uu[q] + dd[q];
@@ -984,29 +1002,57 @@ static inline unsigned chunk_block() { return L > 256 ? L : 256; }
 template <int L>
 static inline int64_t chunks_per_block() { return L >= 256 ? 1 : 256 / L; }
 
-hipError_t launch_local(bool var, bool uz, const void *g, float *m, const float *x_src, float *x,
-                        float *v, float *u, const void *gbar, int64_t n, const Scalars &s, int gt,
-                        hipStream_t st)
+hipError_t launch_local(bool var, int u_in, bool write_u, const void *g, float *m,
+                        const float *x_src, float *x, float *v, float *u, const void *gbar,
+                        int64_t n, const Scalars &s, int gt, hipStream_t st)
 {
     const int64_t n4 = n / 4;
     if (n4 == 0) return hipSuccess;
+    if (!write_u && u_in != U_ZERO) return hipErrorInvalidValue;
     const dim3 grid(grid_for(n4, 256)), block(256);
     return with_grad_type(gt, [&](auto T) {
         constexpr int GT = decltype(T)::value;
-        if (var && uz)
-            hipLaunchKernelGGL((k_local<true, true, GT>), grid, block, 0, st, g, m, x_src, x, v,
-                               u, gbar, n4, s);
-        else if (var)
-            hipLaunchKernelGGL((k_local<true, false, GT>), grid, block, 0, st, g, m, x_src, x, v,
-                               u, gbar, n4, s);
-        else if (uz)
-            hipLaunchKernelGGL((k_local<false, true, GT>), grid, block, 0, st, g, m, x_src, x, v,
-                               u, gbar, n4, s);
-        else
-            hipLaunchKernelGGL((k_local<false, false, GT>), grid, block, 0, st, g, m, x_src, x,
-                               v, u, gbar, n4, s);
-        return hipGetLastError();
+        auto go = [&](auto kernel) {
+            hipLaunchKernelGGL(kernel, grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s);
+            return hipGetLastError();
+        };
+#define ZO_LOCAL(VAR_)                                                                        \
+    switch (u_in * 2 + (write_u ? 1 : 0)) {                                                   \
+    case U_MEM * 2 + 1: return go(k_local<VAR_, U_MEM, true, GT>);                            \
+    case U_ZERO * 2 + 1: return go(k_local<VAR_, U_ZERO, true, GT>);                          \
+    case U_ZERO * 2 + 0: return go(k_local<VAR_, U_ZERO, false, GT>);                         \
+    case U_GM * 2 + 1: return go(k_local<VAR_, U_GM, true, GT>);                              \
+    default: return hipErrorInvalidValue;                                                     \
+    }
+        if (var) {
+            ZO_LOCAL(true)
+        } else {
+            ZO_LOCAL(false)
+        }
+#undef ZO_LOCAL
     });
+}
+
+// u = +0 + gamma_u * m, one float4 per thread.
+__global__ __launch_bounds__(256) void k_u_from_m(float *__restrict__ u,
+                                                  const float *__restrict__ m, int64_t n4,
+                                                  float gamma_u)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n4) return;
+    const f4v mm = ldnt(m, i);
+    f4v r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r[q] = 0.0f + gamma_u * mm[q];
+    stnt(u, i, r);
+}
+
+hipError_t launch_u_from_m(float *u, const float *m, int64_t n, float gamma_u, hipStream_t st)
+{
+    const int64_t n4 = n / 4;
+    if (n4 == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_u_from_m, dim3(grid_for(n4, 256)), dim3(256), 0, st, u, m, n4, gamma_u);
+    return hipGetLastError();
 }
 
 hipError_t launch_zero(float *dst, int64_t n, hipStream_t st)
@@ -1030,33 +1076,32 @@ hipError_t launch_var(float *v, const void *gbar, int64_t n, const Scalars &s, i
     });
 }
 
-hipError_t launch_sync1(Geometry geo, bool fused, bool uz, const void *g, const float *m,
+hipError_t launch_sync1(Geometry geo, bool fused, int u_in, const void *g, const float *m,
                         const void *u, float *err, const Chunks &ch, int64_t nchunks,
                         uint64_t *packed, float *scales, const Scalars &s, int gt, int ut,
                         hipStream_t st)
 {
     if (nchunks == 0) return hipSuccess;
-    if (uz && !fused) return hipErrorInvalidValue;
+    if (u_in != U_MEM && !fused) return hipErrorInvalidValue;
     if (fused && ut != GT_F32) return hipErrorInvalidValue;
     return with_grad_type(fused ? gt : ut, [&](auto T) {
         constexpr int GT = decltype(T)::value;
         return with_geometry(geo, [&](auto Lc, auto Vc) {
             constexpr int L = decltype(Lc)::value, V = decltype(Vc)::value;
-            const unsigned grid = grid_for(nchunks, chunks_per_block<L>());
+            const dim3 grid(grid_for(nchunks, chunks_per_block<L>())), block(chunk_block<L>());
             uint32_t *p32 = reinterpret_cast<uint32_t *>(packed);
-            if (uz)
-                hipLaunchKernelGGL((k_sync1<L, V, true, true, GT>), dim3(grid),
-                                   dim3(chunk_block<L>()), 0, st, g, m, u, err, ch, nchunks, p32,
+            auto go = [&](auto kernel) {
+                hipLaunchKernelGGL(kernel, grid, block, 0, st, g, m, u, err, ch, nchunks, p32,
                                    scales, s);
-            else if (fused)
-                hipLaunchKernelGGL((k_sync1<L, V, true, false, GT>), dim3(grid),
-                                   dim3(chunk_block<L>()), 0, st, g, m, u, err, ch, nchunks, p32,
-                                   scales, s);
-            else
-                hipLaunchKernelGGL((k_sync1<L, V, false, false, GT>), dim3(grid),
-                                   dim3(chunk_block<L>()), 0, st, g, m, u, err, ch, nchunks, p32,
-                                   scales, s);
-            return hipGetLastError();
+                return hipGetLastError();
+            };
+            if (!fused) return go(k_sync1<L, V, false, U_MEM, GT>);
+            switch (u_in) {
+            case U_MEM: return go(k_sync1<L, V, true, U_MEM, GT>);
+            case U_ZERO: return go(k_sync1<L, V, true, U_ZERO, GT>);
+            case U_GM: return go(k_sync1<L, V, true, U_GM, GT>);
+            default: return hipErrorInvalidValue;
+            }
         });
     });
 }

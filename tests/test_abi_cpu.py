@@ -111,7 +111,7 @@ def test_unbuilt_library_raises(monkeypatch, tmp_path):
 def test_state_calls_reject_null_handle():
     lib = zo.lib()
     assert lib.zo_materialize(None) == zo.ZO_EINVAL
-    assert lib.zo_state_location(None, None, None) == zo.ZO_EINVAL
+    assert lib.zo_state_location(None, None, None, None) == zo.ZO_EINVAL
 
 
 def test_config_carries_deferred_writes_flag():

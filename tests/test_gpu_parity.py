@@ -164,20 +164,38 @@ def test_materialize_after_deferred_sync(torch_cuda):
     report, inexact = harness.run_parity(wl, log=_log, defer=True, materialize_at=(1, 3, 5))
     _assert_clean(report, inexact)
     run = harness.GpuRun(wl, defer=True)
+    zo = run.zo
+    n = wl.n
     try:
         for t in range(3):
             run.step(t)
-        xp, uz = run.zo.zo_state_location(run.opt.h)
-        assert xp == run.state["anchor"].data_ptr() and uz
+        # after the sync at step 2: the model in the anchor, u = +0
+        xp, mode, _ = zo.zo_state_location(run.opt.h)
+        assert xp == run.state["anchor"].data_ptr() and mode == zo.U_ZERO
         run.opt.materialize()
-        xp, uz = run.zo.zo_state_location(run.opt.h)
-        assert xp == run.state["x"].data_ptr() and not uz
-        n = wl.n
+        xp, mode, _ = zo.zo_state_location(run.opt.h)
+        assert xp == run.state["x"].data_ptr() and mode == zo.U_IN_BUFFER
         torch.cuda.synchronize()
         assert torch.equal(run.state["x"][:n].view(torch.int32),
                            run.state["anchor"][:n].view(torch.int32))
         assert torch.equal(run.state["u"][:n].view(torch.int32),
                            torch.zeros(n, dtype=torch.int32, device="cuda"))
+        # one more sync, then the first local step after it: u = +0 + gamma_3 m
+        run.step(3)
+        run2 = harness.GpuRun(wl, defer=True)
+        try:
+            for t in range(4):
+                run2.step(t)
+            xp, mode, gam = zo.zo_state_location(run2.opt.h)
+            assert mode == zo.U_GAMMA_M and gam == wl.gamma(3)
+            assert xp == run2.state["x"].data_ptr()
+            run2.opt.materialize()
+            torch.cuda.synchronize()
+            want = (run2.state["m"][:n] * torch.tensor(gam, device="cuda")) + 0.0
+            assert torch.equal(run2.state["u"][:n].view(torch.int32), want.view(torch.int32))
+            assert zo.zo_state_location(run2.opt.h)[1] == zo.U_IN_BUFFER
+        finally:
+            run2.close()
     finally:
         run.close()
 
