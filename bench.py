@@ -27,6 +27,7 @@ import csv
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -42,23 +43,29 @@ COPY_BYTES = 4 << 30          # size of the calibration copies
 # The second template argument of k_local / k_recon is the deferred variant
 # (the very first local step of a run has no sync before it and is skipped).
 def kernel_keys(mode):
-    """Kernel-name prefixes of the timed kernels for a mode ("deferred",
-    "eager" or "frozen-variance", with "/f16" or "/bf16" for 16-bit
-    gradients); the last template argument of the gradient-reading kernels
-    is the gradient type (0 binary32, 1 binary16, 2 bfloat16)."""
-    copies = {"zo::k_copy<true>": ("copy_nt", None), "zo::k_copy<false>": ("copy_plain", None)}
+    """Regular expressions for the names of the timed kernels in a mode
+    ("deferred", "eager" or "frozen-variance", with "/f16" or "/bf16" for
+    16-bit gradients) -> (bench name, access kind).  The last template
+    argument of the gradient-reading kernels is the gradient type (0 binary32,
+    1 binary16, 2 bfloat16); the steady-state variants only (the first local
+    step and compress of a run, before any sync, are other instantiations)."""
+    copies = {r"zo::k_copy<true>": ("copy_nt", None), r"zo::k_copy<false>": ("copy_plain", None)}
     base, _, dt = mode.partition("/")
     gt = {"": 0, "f16": 1, "bf16": 2}[dt]
     if base == "frozen-variance":
-        return {f"zo::k_fv_full<{gt}>": ("fv_full", "nt"), "zo::k_sync1<": ("sync1", "nt"),
-                "zo::k_srv_lut<": ("srv", "plain"), "zo::k_fv_apply": ("fv_apply", "nt")} | copies
+        return {rf"zo::k_fv_full<{gt}>": ("fv_full", "nt"),
+                rf"zo::k_sync1<\d+, \d+, false, 0, {gt}>": ("sync1", "nt"),
+                r"zo::k_srv_lut<": ("srv", "plain"), r"zo::k_fv_apply": ("fv_apply", "nt")} | copies
     dv = "true" if base == "deferred" else "false"
     # k_local<VAR, UIN, WU, GT>: deferred, the local step after a sync has
-    # UIN = 1 (u = +0) and WU = false; eager UIN = 0, WU = true
+    # UIN = 1 (u = +0) and WU = false, and the compress after it UIN = 2
+    # (u = +0 + gamma m); eager UIN = 0 throughout
     lv = f"true, 1, false, {gt}" if base == "deferred" else f"true, 0, true, {gt}"
-    return {f"zo::k_local<{lv}>": ("local+var", "nt"), "zo::k_sync1<": ("sync1", "nt"),
-            "zo::k_srv_lut<": ("srv", "plain"),
-            f"zo::k_recon<true, {dv}, {gt}>": ("recon+var", "nt")} | copies
+    su = 2 if base == "deferred" else 0
+    return {rf"zo::k_local<{lv}>": ("local+var", "nt"),
+            rf"zo::k_sync1<\d+, \d+, true, {su}, {gt}>": ("sync1", "nt"),
+            r"zo::k_srv_lut<": ("srv", "plain"),
+            rf"zo::k_recon<true, {dv}, {gt}>": ("recon+var", "nt")} | copies
 
 
 def source_hash():
@@ -83,8 +90,8 @@ def summarize_pmc(fetch_dir, write_dir, out_path, mode):
                     if r["Counter_Name"] != counter:
                         continue
                     name = r["Kernel_Name"].replace("void ", "")
-                    for prefix, (key, _) in keys.items():
-                        if name.startswith(prefix):
+                    for pattern, (key, _) in keys.items():
+                        if re.match(pattern, name):
                             vals.setdefault(key, []).append(float(r["Counter_Value"]))
         return {k: sum(v) / len(v) for k, v in vals.items()}
     fetch, write = load(fetch_dir, "FETCH_SIZE"), load(write_dir, "WRITE_SIZE")
