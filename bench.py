@@ -9,10 +9,11 @@ optimizer steps that together run every kernel of the path once:
                                        K_srv, W = 128      (zo_unpack_average)
                                        K_recon+var         (zo_sync_update)
 The reconstruction defers its x and u writes (the new model stays in the
-anchor buffer, u is an implicit zero; the next local step writes x but leaves
-u = +0 + gamma m implicit, which the compress forms from the m it reads; same
-values, 20 bytes per parameter less per bench step); --eager-sync-writes times
-the eager variant.
+anchor buffer, u is an implicit zero and m is rebuilt from a 1-bit copy of
+the server output; the next local step writes x and m but leaves u = +0 +
+gamma m implicit, which the compress forms from the m it reads; same values,
+28 bytes per parameter less per bench step); --eager-sync-writes times the
+eager variant.
 Inputs (gradient, averaged gradient, peers' packed signs and scales) are
 generated once on the device before timing and stay resident in HBM.
 `value` is optimizer-step parameter updates per second (2 d per bench step).
@@ -148,23 +149,27 @@ def algorithmic_bytes_fv(d, nchunks, nwords, W, gbytes=4):
 def algorithmic_bytes(d, nchunks, nwords, W, deferred=True, gbytes=4):
     """Bytes each kernel must move per launch: every state read once and
     written once, packed words and per-chunk scales included (gbytes: bytes
-    per gradient element of g and gbar).  With deferred sync writes the local
-    step after a sync reads x from the anchor and neither reads nor writes u
-    (u = +0 + gamma m there), the compress that follows forms u from the m it
-    reads, and the reconstruction writes neither x nor u."""
+    per gradient element of g and gbar).  With deferred sync writes the
+    reconstruction writes neither x, m nor u but copies the server's packed
+    words and scales; the local step after it reads x from the anchor and m
+    from that copy, and neither reads nor writes u (u = +0 + gamma m there);
+    the compress that follows forms u from the m it reads."""
     pk = 8 * nwords
     sc = 4 * nchunks
     return {
-        # reads g, m, x, v, gbar, u (eager only); writes m, x, v, u (eager only)
-        "local+var": ((24 if deferred else 32) + 2 * gbytes) * d,
+        # reads g, gbar, x, v, m (eager; deferred: the server copy), u (eager);
+        # writes m, x, v, u (eager only)
+        "local+var": (32 + 2 * gbytes) * d if not deferred else
+                     (20 + 2 * gbytes) * d + pk + sc,
         # reads g, m, err, u (eager only); writes err, own packed words, own scales
         "sync1": ((12 if deferred else 16) + gbytes) * d + pk + sc,
         # reads W packed buffers + W scale rows + server error;
         # writes server error, server packed words, server scales
         "srv": W * (pk + sc) + 8 * d + pk + sc,
-        # reads server words + scales, v, anchor, gbar; writes m, anchor, v,
-        # and x, u (eager only)
-        "recon+var": pk + sc + ((20 if deferred else 28) + gbytes) * d,
+        # reads server words + scales, v, anchor, gbar; writes anchor, v, and
+        # m, x, u (eager) or the copy of the server words + scales (deferred)
+        "recon+var": pk + sc + (28 + gbytes) * d if not deferred else
+                     2 * (pk + sc) + (16 + gbytes) * d,
     }
 
 
@@ -180,12 +185,12 @@ def stream_mix_ceilings(zo, torch, state, g, gb, d, mode):
         "sync1": ([g, S["err"]], [S["x"]]),
         "fv_apply": ([S["x"], S["m"], S["v"]], [S["u"], S["anchor"]]),
     } if mode == "frozen-variance" else {
-        "local+var": ([g, gb, S["m"], S["anchor"], S["v"]] + ([] if deferred else [S["u"]]),
+        "local+var": ([g, gb, S["anchor"], S["v"]] + ([] if deferred else [S["m"], S["u"]]),
                       [S["x"], S["err"], S["srv_err"]] if deferred else
                       [S["x"], S["err"], S["srv_err"], S["anchor"]]),
         "sync1": ([g, S["m"], S["err"]] + ([] if deferred else [S["u"]]), [S["x"]]),
         "recon+var": ([S["v"], S["anchor"], gb],
-                      [S["m"], S["x"], S["u"]] if deferred else
+                      [S["m"], S["x"]] if deferred else
                       [S["m"], S["x"], S["u"], S["err"]]),
     }
     out = {}

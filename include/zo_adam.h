@@ -93,18 +93,23 @@ typedef struct zo_adam zo_adam;   /* opaque handle */
  *                  server half of Algorithm 2; end < 0 means "to the last
  *                  chunk" (begin = 0, end = -1 is the single server).
  *   defer_sync_writes
- *                  0: zo_sync_update writes x, anchor and u = 0 (x and u are
- *                  always current in their buffers).  Nonzero: it writes only
- *                  m and the anchor (8 bytes per parameter less); the new
- *                  model is then held in `anchor` and u is +0 by definition.
+ *                  0: zo_sync_update writes m, x, anchor and u = 0 (x, m and
+ *                  u are always current in their buffers).  Nonzero: it
+ *                  writes only the anchor (12 bytes per parameter less) and a
+ *                  copy of the server's packed words and scales into the
+ *                  library's own memory (allocated by zo_adam_init): the new
+ *                  model is held in `anchor`, u is +0 by definition and m is
+ *                  the server's average over Gamma, which the next call
+ *                  rebuilds from the 1-bit copy (reading 1/8 byte per
+ *                  parameter instead of 4).
  *                  The next zo_local_step reads the model from the anchor and
- *                  writes x, and neither reads nor writes u (8 bytes less):
+ *                  writes x and m, and neither reads nor writes u (8 bytes less):
  *                  u is then +0 + gamma_t m_{t+1} in binary32, the one
  *                  product it added, so the next call that needs u (a local
  *                  step, which writes it, or a fused compress) forms it from
  *                  the m it reads anyway (4 bytes less).  A local step at a
  *                  sync step (the unfused path) always writes u.
- *                  zo_state_location says where x and u are; zo_materialize
+ *                  zo_read_state gives the current x, m or u; zo_materialize
  *                  writes them out.  The arithmetic, and so every value, is
  *                  the same in both modes.
  *   algorithm      ZO_ALG_ZERO_ONE_ADAM (default 0) or ZO_ALG_FROZEN_VARIANCE.
@@ -260,12 +265,24 @@ int zo_variance_update(zo_adam *h, int64_t t, const void *gbar);
 
 /*
  * zo_materialize -- with defer_sync_writes, write out what is implicit:
- * x <- anchor, and u <- +0 or +0 + gamma m (one copy and one fill kernel on
- * the handle's stream, only for what is pending).  Between steps
+ * x <- anchor, u <- +0 or +0 + gamma m, and m from the server copy (a few
+ * elementwise kernels on the handle's stream, only for what is pending).  Between steps
  * only (ZO_ESTATE otherwise); changes no value of the optimizer state.  The
  * next steps run as after an eager zo_sync_update.
  */
 int zo_materialize(zo_adam *h);
+
+/* State vectors for zo_read_state. */
+enum { ZO_STATE_X = 0, ZO_STATE_M = 1, ZO_STATE_U = 2 };
+
+/*
+ * zo_read_state -- the current value of x, m or u (which = ZO_STATE_*) into
+ * out (device float[n], 16-byte aligned, async on the handle's stream),
+ * wherever deferred sync writes keep it.  Between steps only (ZO_ESTATE
+ * otherwise); changes nothing.  ZO_STATE_U is ZO_EINVAL under
+ * ZO_ALG_FROZEN_VARIANCE (no buffer).
+ */
+int zo_read_state(zo_adam *h, int32_t which, float *out);
 
 /* ---- queries (host only; never touch the device unless stated) ---------- */
 /* Where the current state is: *x_now = the device buffer that holds x

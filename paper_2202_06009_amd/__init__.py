@@ -23,7 +23,8 @@ ALGORITHMS = {"zero-one": ZO_ALG_ZERO_ONE_ADAM, "frozen-variance": ZO_ALG_FROZEN
 EXPORTS = (
     "zo_adam_init", "zo_adam_destroy", "zo_set_stream", "zo_local_step",
     "zo_compress_pack_ef", "zo_unpack_average", "zo_sync_update", "zo_variance_update",
-    "zo_fullprec_step", "zo_materialize", "zo_state_location", "zo_num_chunks", "zo_packed_words",
+    "zo_fullprec_step", "zo_materialize", "zo_state_location", "zo_read_state", "zo_num_chunks",
+    "zo_packed_words",
     "zo_server_range", "zo_chunk_table", "zo_gamma_sum", "zo_next_step", "zo_inexact_chunks",
     "zo_strerror", "zo_last_hip_error", "zo_diag_divsqrt", "zo_diag_copy", "zo_diag_stream",
     "zo_config_check", "zo_plan_num_chunks", "zo_plan_chunks",
@@ -79,6 +80,7 @@ def lib():
             "zo_variance_update": ([vp, i64, vp], ci),
             "zo_materialize": ([vp], ci),
             "zo_fullprec_step": ([vp, i64, f32, vp], ci),
+            "zo_read_state": ([vp, i32, vp], ci),
             "zo_state_location": ([vp, ctypes.POINTER(vp), ctypes.POINTER(i32),
                                    ctypes.POINTER(f32)], ci),
             "zo_num_chunks": ([vp], i64),
@@ -228,6 +230,12 @@ def zo_materialize(h):
 
 
 U_IN_BUFFER, U_ZERO, U_GAMMA_M = 0, 1, 2
+ZO_STATE_X, ZO_STATE_M, ZO_STATE_U = 0, 1, 2
+
+
+def zo_read_state(h, which, out, stream=None):
+    """The current x / m / u (which = ZO_STATE_*) into the device tensor out."""
+    _call(h, "zo_read_state", int(which), _ptr(out))
 
 
 def zo_state_location(h):
@@ -331,21 +339,14 @@ class ZoAdam:
         zo_materialize(self.h)
 
     def current(self, name):
-        """The tensor holding state `name` now (x may live in the anchor after a
-        deferred sync; u then reads as zeros)."""
-        if self.cfg["algorithm"] != "zero-one":
+        """State `name` as it is now: x, m and u through zo_read_state (deferred
+        sync writes may keep them elsewhere), the others from their buffers."""
+        which = {"x": ZO_STATE_X, "m": ZO_STATE_M, "u": ZO_STATE_U}.get(name)
+        if which is None or (name == "u" and self.cfg["algorithm"] != "zero-one"):
             return self.state[name]
-        xp, mode, gam = zo_state_location(self.h)
-        if name == "x" and xp == self.state["anchor"].data_ptr():
-            return self.state["anchor"]
-        if name == "u" and mode == U_ZERO:
-            return self.state["u"].new_zeros(self.state["u"].shape)
-        if name == "u" and mode == U_GAMMA_M:
-            # the library's definition, binary32: +0 + gamma * m (view only)
-            import torch
-            g32 = torch.tensor(gam, dtype=torch.float32, device=self.state["m"].device)
-            return (self.state["m"] * g32) + 0.0
-        return self.state[name]
+        out = self.state[name].new_empty(self.state[name].shape)
+        zo_read_state(self.h, which, out)
+        return out
 
     # queries
     @property

@@ -79,6 +79,9 @@ struct zo_adam {
     bool defer = false, x_in_anchor = false;
     int u_in = zo::U_MEM;
     float gamma_u = 0.0f;
+    // deferred mode: the copy of the last server output the momentum is
+    // rebuilt from while u_in == U_ZERO (allocated with the chunk table)
+    zo::SrvCopy sm{};
     // Algorithm 4 instead of Algorithm 1; fv_gamma = gamma_t of the step whose
     // compressed average zo_sync_update applies.
     bool fv = false;
@@ -223,9 +226,12 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
         h->e0 = h->e1 = h->w0 = h->w1 = 0;
     }
 
-    // Device chunk table + per-chunk exactness flags: the only allocations.
+    // Device chunk table + per-chunk exactness flags (+ in deferred mode the
+    // server-output copy: packed words and scales): the only allocations.
     const size_t nb = (size_t)h->nchunks;
-    const size_t bytes = nb * (8 + 8 + 4) + (size_t)(h->c1 - h->c0) + 64;
+    const size_t copy_off = (nb * (8 + 8 + 4) + (size_t)(h->c1 - h->c0) + 64 + 255) & ~(size_t)255;
+    const size_t copy_bytes = h->defer ? (size_t)h->nwords * 8 + nb * 4 : 0;
+    const size_t bytes = copy_off + copy_bytes;
     if (nb) {
         hipError_t e = hipMalloc(&h->dtable, bytes);
         if (e != hipSuccess) {
@@ -238,6 +244,10 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
         h->ch.word = (const int64_t *)(base + nb * 8);
         h->ch.len = (const int32_t *)(base + nb * 16);
         h->dflags = (uint8_t *)(base + nb * 20);
+        if (h->defer) {
+            h->sm.words32 = (uint32_t *)(base + copy_off);
+            h->sm.scales = (float *)(base + copy_off + (size_t)h->nwords * 8);
+        }
         hipError_t e1 = hipMemcpyAsync(base, h->hstart.data(), nb * 8, hipMemcpyHostToDevice,
                                        stream);
         hipError_t e2 = hipMemcpyAsync(base + nb * 8, h->hword.data(), nb * 8,
@@ -319,7 +329,8 @@ int zo_local_step(zo_adam *h, int64_t t, float gamma, const void *g, const void 
     const bool write_u = !(h->u_in == zo::U_ZERO && !tu);
     s.gamma_u = h->gamma_u;
     hipError_t e = zo::launch_local(gbar != nullptr, h->u_in, write_u, g, h->st.m, x_src,
-                                    h->st.x, h->st.v, h->st.u, gbar, h->n, s, h->gt, h->stream);
+                                    h->st.x, h->st.v, h->st.u, gbar, h->n, s, h->gt, h->ch,
+                                    h->nchunks, h->chunk, h->sm, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     h->x_in_anchor = false;
     if (write_u) {
@@ -353,7 +364,7 @@ int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const void *g, uint6
         zo::Scalars s = h->sc;
         hipError_t e = zo::launch_sync1(h->geo, false, zo::U_MEM, nullptr, nullptr, g, h->st.err,
                                         h->ch, h->nchunks, packed0, scales0, s, zo::GT_F32,
-                                        h->gt, h->stream);
+                                        h->gt, h->sm, h->stream);
         if (e != hipSuccess) return h->hip_fail(e);
         h->fv_gamma = gamma;
         h->phase = PH_COMPRESSED;
@@ -374,7 +385,7 @@ int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const void *g, uint6
     // unfused path)
     hipError_t e = zo::launch_sync1(h->geo, fused, fused ? h->u_in : zo::U_MEM, g, h->st.m,
                                     h->st.u, h->st.err, h->ch, h->nchunks, packed0, scales0, s,
-                                    h->gt, zo::GT_F32, h->stream);
+                                    h->gt, zo::GT_F32, h->sm, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     if (fused) h->gamma_sum = h->gamma_sum + gamma;
     h->phase = PH_COMPRESSED;
@@ -421,14 +432,17 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
     const bool tv = h->in_tv(t);
     if (gbar && !tv) return ZO_EINVAL;
     // the deferred kernel reads the anchor, which holds x_{t'} in both cases
+    zo::SrvCopy sm = h->sm;
+    sm.gamma_m = h->gamma_sum;
     hipError_t e = zo::launch_recon(h->geo, gbar != nullptr, h->defer, srv_packed, srv_scales,
                                     h->ch, h->nchunks, h->st.m, h->st.x, h->st.v, h->st.u,
-                                    h->st.anchor, gbar, h->gamma_sum, h->sc, h->gt, h->chunk,
+                                    h->st.anchor, gbar, h->gamma_sum, h->sc, h->gt, h->chunk, sm,
                                     h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     if (h->defer) {
         h->x_in_anchor = true;
         h->u_in = zo::U_ZERO;
+        h->sm.gamma_m = h->gamma_sum;
     }
     h->gamma_sum = 0.0f;
     if (tv && !gbar)
@@ -474,6 +488,31 @@ int zo_state_location(const zo_adam *h, float **x_now, int32_t *u_mode, float *u
     return ZO_OK;
 }
 
+int zo_read_state(zo_adam *h, int32_t which, float *out)
+{
+    if (!h) return ZO_EINVAL;
+    if (which != ZO_STATE_X && which != ZO_STATE_M && which != ZO_STATE_U) return ZO_EINVAL;
+    if (which == ZO_STATE_U && h->fv) return ZO_EINVAL;
+    if (h->n > 0 && !out) return ZO_EINVAL;
+    if (!aligned(out, 16)) return ZO_EALIGN;
+    if (h->phase != PH_IDLE) return ZO_ESTATE;
+    hipError_t e = hipSuccess;
+    if (which == ZO_STATE_X) {
+        e = zo::launch_copy(h->x_in_anchor ? h->st.anchor : h->st.x, out, h->n, true, h->stream);
+    } else if (which == ZO_STATE_M) {
+        e = h->u_in == zo::U_ZERO
+                ? zo::launch_m_from_copy(out, h->ch, h->nchunks, h->chunk, h->sm, h->stream)
+                : zo::launch_copy(h->st.m, out, h->n, true, h->stream);
+    } else if (h->u_in == zo::U_ZERO) {
+        e = zo::launch_zero(out, h->n, h->stream);
+    } else if (h->u_in == zo::U_GM) {
+        e = zo::launch_u_from_m(out, h->st.m, h->n, h->gamma_u, h->stream);
+    } else {
+        e = zo::launch_copy(h->st.u, out, h->n, true, h->stream);
+    }
+    return e == hipSuccess ? ZO_OK : h->hip_fail(e);
+}
+
 int zo_materialize(zo_adam *h)
 {
     if (!h || h->fv) return ZO_EINVAL;
@@ -485,6 +524,8 @@ int zo_materialize(zo_adam *h)
     h->x_in_anchor = false;
     if (h->u_in == zo::U_ZERO) {
         hipError_t e = zo::launch_zero(h->st.u, h->n, h->stream);
+        if (e == hipSuccess)
+            e = zo::launch_m_from_copy(h->st.m, h->ch, h->nchunks, h->chunk, h->sm, h->stream);
         if (e != hipSuccess) return h->hip_fail(e);
     } else if (h->u_in == zo::U_GM) {
         hipError_t e = zo::launch_u_from_m(h->st.u, h->st.m, h->n, h->gamma_u, h->stream);

@@ -13,11 +13,28 @@ struct Scalars {
     float gamma_u;  // U_GM: the buffer is +0 + gamma_u * m (see BufferIn)
 };
 
-// Where a kernel finds the buffer u.  U_MEM: in memory.  U_ZERO: +0 (reset by
-// the last synchronisation, not yet written).  U_GM: u = +0 + gamma_u * m with
-// m the momentum before this step (the only local step since the reset ran
-// with gamma_u and wrote m; binary32, so the product is the value it added).
+// Where a kernel finds the buffer u (and, after a deferred reconstruction, the
+// momentum).  U_MEM: u and m in memory.  U_ZERO: the state a deferred
+// reconstruction leaves: u = +0, and m = (sign bit ? S_c : -S_c) / gamma_m from
+// the library's copy of that server output (SrvCopy).  U_GM: u = +0 + gamma_u
+// * m with m in memory, the momentum before this step (the only local step
+// since the reset ran with gamma_u and wrote m; binary32, so the product is
+// the value it added).
 enum BufferIn { U_MEM = 0, U_ZERO = 1, U_GM = 2 };
+
+// The library's copy of the last server output in deferred mode (packed sign
+// words indexed like the shard's, one scale per chunk) and the learning-rate
+// sum Gamma it was divided by.
+struct SrvCopy {
+    uint32_t *words32;
+    float *scales;
+    float gamma_m;
+};
+
+// Grid of the chunk-mapped elementwise kernels: bpc 256-thread workgroups per
+// chunk of more than 1024 elements, else several chunks of lb lanes per
+// workgroup.  Returns the workgroup count.
+int64_t chunk_slots(int chunk, int64_t nchunks, int &bpc, int &lb);
 
 // Device chunk table: start element, length, first packed word.
 struct Chunks {
@@ -42,11 +59,16 @@ enum GradType { GT_F32 = 0, GT_F16 = 1, GT_BF16 = 2 };
 // Server-average algorithm.
 enum SrvAlgo { SRV_AUTO = 0, SRV_PLAIN = 1 };
 
-// u_in: where u is (BufferIn); write_u: false only with U_ZERO, leaving
-// u = gamma * m implicit; x_src may equal x.
+// u_in: where u is (BufferIn; U_ZERO also takes m from `sm`, over the chunk
+// grid); write_u: false only with U_ZERO, leaving u = gamma * m implicit;
+// x_src may equal x.
 hipError_t launch_local(bool var, int u_in, bool write_u, const void *g, float *m,
                         const float *x_src, float *x, float *v, float *u, const void *gbar,
-                        int64_t n, const Scalars &s, int gt, hipStream_t st);
+                        int64_t n, const Scalars &s, int gt, const Chunks &ch, int64_t nchunks,
+                        int chunk, const SrvCopy &sm, hipStream_t st);
+// m = (bit ? S_c : -S_c) / gamma_m from the server copy, over the shard.
+hipError_t launch_m_from_copy(float *m, const Chunks &ch, int64_t nchunks, int chunk,
+                              const SrvCopy &sm, hipStream_t st);
 // u = +0 + gamma_u * m (writes out an implicit U_GM buffer).
 hipError_t launch_u_from_m(float *u, const float *m, int64_t n, float gamma_u, hipStream_t st);
 hipError_t launch_zero(float *dst, int64_t n, hipStream_t st);
@@ -58,17 +80,19 @@ hipError_t launch_var(float *v, const void *gbar, int64_t n, const Scalars &s, i
 hipError_t launch_sync1(Geometry geo, bool fused, int u_in, const void *g, const float *m,
                         const void *u, float *err, const Chunks &ch, int64_t nchunks,
                         uint64_t *packed, float *scales, const Scalars &s, int gt, int ut,
-                        hipStream_t st);
+                        const SrvCopy &sm, hipStream_t st);
 hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const float *scales, int W,
                       int64_t wstride, int64_t cstride, const Chunks &ch, int64_t c0,
                       int64_t nch, int64_t word0, int64_t elem0, float *srv_err,
                       uint64_t *srv_packed, float *srv_scales, float *avg, uint8_t *flags,
                       int chunk, hipStream_t st);
-// defer: write m and anchor only (the model stays in the anchor, u = 0 implicit).
+// defer: write the anchor and `sm` only (the model stays in the anchor, u = 0
+// and m = the server average / Gamma implicit).
 hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const void *gbar,
-                        float gsum, const Scalars &s, int gt, int chunk, hipStream_t st);
+                        float gsum, const Scalars &s, int gt, int chunk, const SrvCopy &sm,
+                        hipStream_t st);
 // Algorithm 4: the full-precision step (t in T_v) and the step from the
 // server's compressed average (t outside T_v).
 hipError_t launch_fv_full(const void *gbar, float *x, float *m, float *v, int64_t n,

@@ -124,6 +124,34 @@ __device__ __forceinline__ float var_elem(float v, float gb, const Scalars &s)
 // a1 (+a2): local step, one float4 per thread
 // ---------------------------------------------------------------------------
 
+// The chunk c and the offset e (a multiple of 4) in it of this thread's
+// float4; false when the thread has none.
+__device__ __forceinline__ bool chunk_slot(Chunks ch, int64_t nchunks, int bpc, int lb,
+                                           int64_t &c, int &e)
+{
+    if (bpc > 1) {
+        c = (int64_t)blockIdx.x / bpc;
+        e = 1024 * (int)(blockIdx.x - c * bpc) + 4 * (int)threadIdx.x;
+    } else {
+        c = (int64_t)blockIdx.x * (256 / lb) + threadIdx.x / lb;
+        e = 4 * (int)(threadIdx.x % lb);
+    }
+    return c < nchunks && e < ch.len[c];
+}
+
+// The momentum of float4 e/4 of chunk c after a deferred reconstruction:
+// (sign bit ? S_c : -S_c) / Gamma from the library's copy of the server output
+// (the reconstruction's own expression).
+__device__ __forceinline__ f4v m_from_copy(const SrvCopy &sm, const Chunks &ch, int64_t c, int e)
+{
+    const uint32_t bits = sm.words32[2 * ch.word[c] + (e >> 5)] >> (e & 31);
+    const float sc = sm.scales[c];
+    f4v r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r[q] = (((bits >> q) & 1u) ? sc : -sc) / sm.gamma_m;
+    return r;
+}
+
 // The buffer before this step, per BufferIn (m_old: the momentum read).
 template <int UIN>
 __device__ __forceinline__ f4v buffer_in(const float *u, int64_t i4, f4v m_old, const Scalars &s)
@@ -144,16 +172,30 @@ __device__ __forceinline__ f4v buffer_in(const float *u, int64_t i4, f4v m_old, 
 // synchronisation left the model there) and written to x.  UIN: where u is
 // (BufferIn).  WU: write u (false only with U_ZERO: the new u = +0 + gamma m'
 // is then left implicit, U_GM for the next call).
+// UIN = U_ZERO runs over the chunk grid (chunk_slot) and takes m from the
+// server copy; the other variants run one float4 per thread over the shard.
 template <bool VAR, int UIN, bool WU, int GT>
 __global__ __launch_bounds__(256) void k_local(const void *__restrict__ g, float *__restrict__ m,
                                                const float *x_src, float *x,
                                                float *__restrict__ v, float *__restrict__ u,
                                                const void *__restrict__ gbar, int64_t n4,
-                                               Scalars s)
+                                               Scalars s, Chunks ch, int64_t nchunks, int bpc,
+                                               int lb, SrvCopy sm)
 {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n4) return;
-    f4v gg = ldg4<GT>(g, i), mm = ldnt(m, i), xx = ldnt(x_src, i), vv = ldnt(v, i);
+    int64_t i;
+    f4v mm;
+    if constexpr (UIN == U_ZERO) {
+        int64_t c;
+        int e;
+        if (!chunk_slot(ch, nchunks, bpc, lb, c, e)) return;
+        i = (ch.start[c] + e) >> 2;
+        mm = m_from_copy(sm, ch, c, e);
+    } else {
+        i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+        if (i >= n4) return;
+        mm = ldnt(m, i);
+    }
+    f4v gg = ldg4<GT>(g, i), xx = ldnt(x_src, i), vv = ldnt(v, i);
     f4v uu = buffer_in<UIN>(u, i, mm, s);
     f4v gb;
     if (VAR) gb = ldg4<GT>(gbar, i);
@@ -336,7 +378,7 @@ template <int L, int V, bool FUSED, int UIN, int GT>
 __global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
     const void *__restrict__ g, const float *__restrict__ m, const void *__restrict__ u,
     float *__restrict__ err, Chunks ch, int64_t nchunks, uint32_t *__restrict__ packed32,
-    float *__restrict__ scales, Scalars s)
+    float *__restrict__ scales, Scalars s, SrvCopy sm)
 {
     __shared__ float lds[64];
     constexpr int CPW = L >= 256 ? 1 : 256 / L;
@@ -355,7 +397,8 @@ __global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
             const f4v dd = ldnt(err, i4);
             f4v uu;
             if (FUSED) {
-                const f4v gg = ldg4<GT>(g, i4), mm = ldnt(m, i4);
+                const f4v gg = ldg4<GT>(g, i4);
+                const f4v mm = UIN == U_ZERO ? m_from_copy(sm, ch, c, e) : ldnt(m, i4);
                 uu = buffer_in<UIN>(static_cast<const float *>(u), i4, mm, s);
 #pragma unroll
                 for (int q = 0; q < 4; ++q) uu[q] = uu[q] + s.gamma * (s.b1 * mm[q] + s.c1 * gg[q]);
@@ -762,20 +805,6 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
 
 // DEFER: only m and the anchor are written; the new model is the new anchor
 // and u is +0, both left implicit until the next local step writes them.
-// The chunk c and the offset e (a multiple of 4) in it of this thread's
-// float4; false when the thread has none.
-__device__ __forceinline__ bool chunk_slot(Chunks ch, int64_t nchunks, int bpc, int lb,
-                                           int64_t &c, int &e)
-{
-    if (bpc > 1) {
-        c = (int64_t)blockIdx.x / bpc;
-        e = 1024 * (int)(blockIdx.x - c * bpc) + 4 * (int)threadIdx.x;
-    } else {
-        c = (int64_t)blockIdx.x * (256 / lb) + threadIdx.x / lb;
-        e = 4 * (int)(threadIdx.x % lb);
-    }
-    return c < nchunks && e < ch.len[c];
-}
 
 template <bool VAR, bool DEFER, int GT>
 __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_packed32,
@@ -785,14 +814,21 @@ __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_
                                                float *__restrict__ v, float *__restrict__ u,
                                                float *__restrict__ anchor,
                                                const void *__restrict__ gbar, float gsum,
-                                               Scalars s)
+                                               Scalars s, SrvCopy sm)
 {
     int64_t c;
     int e;
     if (!chunk_slot(ch, nchunks, bpc, lb, c, e)) return;
     const int64_t i4 = (ch.start[c] + e) >> 2;
     const float sc = srv_scales[c];
-    const uint32_t bits = srv_packed32[2 * ch.word[c] + (e >> 5)] >> (e & 31);
+    const int64_t wd = 2 * ch.word[c] + (e >> 5);
+    const uint32_t dw = srv_packed32[wd];
+    const uint32_t bits = dw >> (e & 31);
+    if (DEFER) {
+        // the copy the next step rebuilds m from (one thread per dword)
+        if ((e & 31) == 0) sm.words32[wd] = dw;
+        if (e == 0) sm.scales[c] = sc;
+    }
     const f4v vv = ldnt(v, i4), an = ldnt(anchor, i4);
     f4v gb;
     if (VAR) gb = ldg4<GT>(gbar, i4);
@@ -804,9 +840,9 @@ __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_
         xx[q] = an[q] - ub / sqrtf(vv[q] + s.eps);
         if (VAR) nv[q] = var_elem(vv[q], gb[q], s);
     }
-    stnt(m, i4, mm);
     stnt(anchor, i4, xx);
     if (!DEFER) {
+        stnt(m, i4, mm);
         stnt(x, i4, xx);
         stnt(u, i4, f4v{0.f, 0.f, 0.f, 0.f});
     }
@@ -1002,18 +1038,40 @@ static inline unsigned chunk_block() { return L > 256 ? L : 256; }
 template <int L>
 static inline int64_t chunks_per_block() { return L >= 256 ? 1 : 256 / L; }
 
+// Grid of the chunk-mapped elementwise kernels (see chunk_slot): bpc
+// 256-thread workgroups per chunk of more than 1024 elements, else several
+// chunks of lb lanes per workgroup.
+int64_t chunk_slots(int chunk, int64_t nchunks, int &bpc, int &lb)
+{
+    const int lanes = (chunk + 3) / 4;
+    if (lanes > 256) {
+        bpc = (lanes + 255) / 256;
+        lb = 256;
+        return nchunks * bpc;
+    }
+    bpc = 1;
+    lb = next_pow2(lanes);
+    return (nchunks + (256 / lb) - 1) / (256 / lb);
+}
+
 hipError_t launch_local(bool var, int u_in, bool write_u, const void *g, float *m,
                         const float *x_src, float *x, float *v, float *u, const void *gbar,
-                        int64_t n, const Scalars &s, int gt, hipStream_t st)
+                        int64_t n, const Scalars &s, int gt, const Chunks &ch, int64_t nchunks,
+                        int chunk, const SrvCopy &sm, hipStream_t st)
 {
     const int64_t n4 = n / 4;
     if (n4 == 0) return hipSuccess;
     if (!write_u && u_in != U_ZERO) return hipErrorInvalidValue;
-    const dim3 grid(grid_for(n4, 256)), block(256);
+    int bpc = 1, lb = 1;
+    // U_ZERO: the chunk grid; otherwise one float4 per thread
+    const int64_t blocks = u_in == U_ZERO ? chunk_slots(chunk, nchunks, bpc, lb) : grid_for(n4, 256);
+    if (blocks == 0) return hipSuccess;
+    const dim3 grid((unsigned)blocks), block(256);
     return with_grad_type(gt, [&](auto T) {
         constexpr int GT = decltype(T)::value;
         auto go = [&](auto kernel) {
-            hipLaunchKernelGGL(kernel, grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s);
+            hipLaunchKernelGGL(kernel, grid, block, 0, st, g, m, x_src, x, v, u, gbar, n4, s, ch,
+                               nchunks, bpc, lb, sm);
             return hipGetLastError();
         };
 #define ZO_LOCAL(VAR_)                                                                        \
@@ -1031,6 +1089,28 @@ hipError_t launch_local(bool var, int u_in, bool write_u, const void *g, float *
         }
 #undef ZO_LOCAL
     });
+}
+
+// m = (bit ? S_c : -S_c) / Gamma from the server copy, over the chunk grid.
+__global__ __launch_bounds__(256) void k_m_from_copy(float *__restrict__ m, Chunks ch,
+                                                     int64_t nchunks, int bpc, int lb,
+                                                     SrvCopy sm)
+{
+    int64_t c;
+    int e;
+    if (!chunk_slot(ch, nchunks, bpc, lb, c, e)) return;
+    stnt(m, (ch.start[c] + e) >> 2, m_from_copy(sm, ch, c, e));
+}
+
+hipError_t launch_m_from_copy(float *m, const Chunks &ch, int64_t nchunks, int chunk,
+                              const SrvCopy &sm, hipStream_t st)
+{
+    if (nchunks == 0) return hipSuccess;
+    int bpc, lb;
+    const int64_t blocks = chunk_slots(chunk, nchunks, bpc, lb);
+    hipLaunchKernelGGL(k_m_from_copy, dim3((unsigned)blocks), dim3(256), 0, st, m, ch, nchunks,
+                       bpc, lb, sm);
+    return hipGetLastError();
 }
 
 // u = +0 + gamma_u * m, one float4 per thread.
@@ -1079,7 +1159,7 @@ hipError_t launch_var(float *v, const void *gbar, int64_t n, const Scalars &s, i
 hipError_t launch_sync1(Geometry geo, bool fused, int u_in, const void *g, const float *m,
                         const void *u, float *err, const Chunks &ch, int64_t nchunks,
                         uint64_t *packed, float *scales, const Scalars &s, int gt, int ut,
-                        hipStream_t st)
+                        const SrvCopy &sm, hipStream_t st)
 {
     if (nchunks == 0) return hipSuccess;
     if (u_in != U_MEM && !fused) return hipErrorInvalidValue;
@@ -1092,7 +1172,7 @@ hipError_t launch_sync1(Geometry geo, bool fused, int u_in, const void *g, const
             uint32_t *p32 = reinterpret_cast<uint32_t *>(packed);
             auto go = [&](auto kernel) {
                 hipLaunchKernelGGL(kernel, grid, block, 0, st, g, m, u, err, ch, nchunks, p32,
-                                   scales, s);
+                                   scales, s, sm);
                 return hipGetLastError();
             };
             if (!fused) return go(k_sync1<L, V, false, U_MEM, GT>);
@@ -1188,21 +1268,6 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
     }
 }
 
-// Grid of the chunk-mapped elementwise kernels (see chunk_slot): bpc
-// 256-thread workgroups per chunk of more than 1024 elements, else several
-// chunks of lb lanes per workgroup.
-static int64_t chunk_slots(int chunk, int64_t nchunks, int &bpc, int &lb)
-{
-    const int lanes = (chunk + 3) / 4;
-    if (lanes > 256) {
-        bpc = (lanes + 255) / 256;
-        lb = 256;
-        return nchunks * bpc;
-    }
-    bpc = 1;
-    lb = next_pow2(lanes);
-    return (nchunks + (256 / lb) - 1) / (256 / lb);
-}
 
 hipError_t launch_fv_full(const void *gbar, float *x, float *m, float *v, int64_t n,
                           const Scalars &s, int gt, hipStream_t st)
@@ -1233,7 +1298,8 @@ hipError_t launch_fv_apply(const uint64_t *srv_packed, const float *srv_scales, 
 hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const void *gbar,
-                        float gsum, const Scalars &s, int gt, int chunk, hipStream_t st)
+                        float gsum, const Scalars &s, int gt, int chunk, const SrvCopy &sm,
+                        hipStream_t st)
 {
     (void)geo;
     if (nchunks == 0) return hipSuccess;
@@ -1245,16 +1311,16 @@ hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_
         constexpr int GT = decltype(T)::value;
         if (var && defer)
             hipLaunchKernelGGL((k_recon<true, true, GT>), g3, b3, 0, st, p32, srv_scales, ch,
-                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s, sm);
         else if (var)
             hipLaunchKernelGGL((k_recon<true, false, GT>), g3, b3, 0, st, p32, srv_scales, ch,
-                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s, sm);
         else if (defer)
             hipLaunchKernelGGL((k_recon<false, true, GT>), g3, b3, 0, st, p32, srv_scales, ch,
-                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s, sm);
         else
             hipLaunchKernelGGL((k_recon<false, false, GT>), g3, b3, 0, st, p32, srv_scales, ch,
-                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s);
+                               nchunks, bpc, lb, m, x, v, u, anchor, gbar, gsum, s, sm);
         return hipGetLastError();
     });
 }
