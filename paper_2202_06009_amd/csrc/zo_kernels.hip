@@ -319,15 +319,18 @@ __device__ __forceinline__ float ef_elem(float a, float s)
 // Equation 3 with error feedback on one chunk whose values `a` are in the
 // lanes' registers (zeros beyond `len`): writes the new error, the packed
 // signs (all 2*ceil(len/64) dwords of the chunk) and the scale.
-template <int L, int V>
-__device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, bool active,
-                                               float *__restrict__ err, int64_t err_e0,
-                                               uint32_t *__restrict__ words32, float *scale_out,
-                                               float *lds)
+// get_a(k) returns block k of a (from registers or from where the caller
+// stashed it); part[k] = abs4 of it, formed by the caller.
+template <int L, int V, class GetA>
+__device__ __forceinline__ void compress_chunk_from(const float (&part_in)[V], GetA get_a, int lc,
+                                                    int len, bool active,
+                                                    float *__restrict__ err, int64_t err_e0,
+                                                    uint32_t *__restrict__ words32,
+                                                    float *scale_out, float *lds)
 {
     float part[V];
 #pragma unroll
-    for (int k = 0; k < V; ++k) part[k] = abs4(a[k]);
+    for (int k = 0; k < V; ++k) part[k] = part_in[k];
     const float tot = chunk_tree<L, V>(part, lds);
     const float s = tot / (float)len;
     const int ndw = 2 * ((len + 63) >> 6);
@@ -338,11 +341,12 @@ __device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, boo
         const bool valid = active && e < len;
         uint32_t nib = 0;
         if (valid) {
+            const f4v ak = get_a(k);
             f4v d;
 #pragma unroll
-            for (int c = 0; c < 4; ++c) d[c] = ef_elem(a[k][c], s);
+            for (int c = 0; c < 4; ++c) d[c] = ef_elem(ak[c], s);
             stnt(err, (err_e0 + e) >> 2, d);
-            nib = sign4(a[k]);
+            nib = sign4(ak);
         }
         const uint32_t dw = wave_or8<L>(nib << (4 * (lc & 7)));
         if constexpr (L >= 8) {
@@ -366,6 +370,19 @@ __device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, boo
     if (active && lc == 0) *scale_out = s;
 }
 
+template <int L, int V>
+__device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, bool active,
+                                               float *__restrict__ err, int64_t err_e0,
+                                               uint32_t *__restrict__ words32, float *scale_out,
+                                               float *lds)
+{
+    float part[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k) part[k] = abs4(a[k]);
+    compress_chunk_from<L, V>(part, [&](int k) { return a[k]; }, lc, len, active, err, err_e0,
+                              words32, scale_out, lds);
+}
+
 // ---------------------------------------------------------------------------
 // a3: worker compress + error feedback + pack (fused with the momentum and
 // buffer lines when g != nullptr)
@@ -375,23 +392,29 @@ __device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, boo
 // type of g when FUSED, else of u (binary32 u, or the gradient itself under
 // Algorithm 4).
 template <int L, int V, bool FUSED, int UIN, int GT>
-__global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
+__global__ __launch_bounds__(L > 256 ? L : 256, V > 1 ? 8 : 1) void k_sync1(
     const void *__restrict__ g, const float *__restrict__ m, const void *__restrict__ u,
     float *__restrict__ err, Chunks ch, int64_t nchunks, uint32_t *__restrict__ packed32,
     float *__restrict__ scales, Scalars s, SrvCopy sm)
 {
     __shared__ float lds[64];
+    // With several blocks per lane, a is parked in LDS across the chunk's
+    // reduction instead of in registers: that keeps a 1024-lane chunk within
+    // 64 registers, so two chunks share a CU.
+    constexpr bool kStash = V > 1;
+    __shared__ f4v stash[kStash ? L * V : 1];
     constexpr int CPW = L >= 256 ? 1 : 256 / L;
     const int lc = threadIdx.x % L;
     const int64_t c = (int64_t)blockIdx.x * CPW + threadIdx.x / L;
     const bool active = c < nchunks;
     const int len = active ? ch.len[c] : 0;
     const int64_t e0 = active ? ch.start[c] : 0;
-    f4v a[V];
+    f4v a[kStash ? 1 : V];
+    float part[V];
 #pragma unroll
     for (int k = 0; k < V; ++k) {
         const int e = 4 * L * k + 4 * lc;
-        a[k] = f4v{0.f, 0.f, 0.f, 0.f};
+        f4v ak = f4v{0.f, 0.f, 0.f, 0.f};
         if (e < len) {
             const int64_t i4 = (e0 + e) >> 2;
             const f4v dd = ldnt(err, i4);
@@ -406,11 +429,17 @@ __global__ __launch_bounds__(L > 256 ? L : 256) void k_sync1(
                 uu = ldg4<GT>(u, i4);
             }
 #pragma unroll
-            for (int q = 0; q < 4; ++q) a[k][q] = uu[q] + dd[q];
+            for (int q = 0; q < 4; ++q) ak[q] = uu[q] + dd[q];
         }
+        part[k] = abs4(ak);
+        if constexpr (kStash)
+            stash[k * L + lc] = ak;
+        else
+            a[k] = ak;
     }
-    compress_chunk<L, V>(a, lc, len, active, err, e0, packed32 + 2 * (active ? ch.word[c] : 0),
-                         scales + (active ? c : 0), lds);
+    compress_chunk_from<L, V>(
+        part, [&](int k) { return kStash ? stash[k * L + lc] : a[kStash ? 0 : k]; }, lc, len,
+        active, err, e0, packed32 + 2 * (active ? ch.word[c] : 0), scales + (active ? c : 0), lds);
 }
 
 // ---------------------------------------------------------------------------
