@@ -177,21 +177,30 @@ def stream_mix_ceilings(zo, torch, state, g, gb, d, mode):
     """HBM rate of a plain streaming kernel (zo_diag_stream) with each hot
     kernel's mix of full-length arrays, on the bench's own buffers (used as
     scratch after the timed region): the rate such a mix can reach on this
-    GPU.  The server's row-strided packed reads have no such plain mix."""
+    GPU.  An array the kernel reads and rewrites (v, the error buffers, the
+    anchor) is a source and a destination of the mix, so it is updated in
+    place as in the kernel; the other arrays are read-only or write-only.  The
+    server's row-strided packed reads have no such plain mix."""
     S = state
     deferred = mode == "deferred"
+    x, m, v, u, err, anchor = (S[k] for k in ("x", "m", "v", "u", "err", "anchor"))
     mixes = {
-        "fv_full": ([gb, S["x"], S["m"], S["v"]], [S["u"], S["err"], S["srv_err"]]),
-        "sync1": ([g, S["err"]], [S["x"]]),
-        "fv_apply": ([S["x"], S["m"], S["v"]], [S["u"], S["anchor"]]),
+        # reads gbar, x, m, v; rewrites x, m, v
+        "fv_full": ([gb, x, m, v], [x, m, v]),
+        # reads g, err; rewrites err
+        "sync1": ([g, err], [err]),
+        # reads x, m, v; rewrites x, m
+        "fv_apply": ([x, m, v], [x, m]),
     } if mode == "frozen-variance" else {
-        "local+var": ([g, gb, S["anchor"], S["v"]] + ([] if deferred else [S["m"], S["u"]]),
-                      [S["x"], S["err"], S["srv_err"]] if deferred else
-                      [S["x"], S["err"], S["srv_err"], S["anchor"]]),
-        "sync1": ([g, S["m"], S["err"]] + ([] if deferred else [S["u"]]), [S["x"]]),
-        "recon+var": ([S["v"], S["anchor"], gb],
-                      [S["m"], S["x"]] if deferred else
-                      [S["m"], S["x"], S["u"], S["err"]]),
+        # deferred: reads g, gbar, the anchor, v; writes m and x, rewrites v.
+        # eager: reads g, gbar, x, v, m, u; rewrites all four states
+        "local+var": ([g, gb, anchor, v], [m, x, v]) if deferred else
+                     ([g, gb, x, v, m, u], [x, v, m, u]),
+        # reads g, m, err (and u, eager); rewrites err
+        "sync1": ([g, m, err] + ([] if deferred else [u]), [err]),
+        # reads v, the anchor, gbar; rewrites the anchor and v (and writes m,
+        # x, u, eager)
+        "recon+var": ([v, anchor, gb], [anchor, v] + ([] if deferred else [m, x, u])),
     }
     out = {}
     for name, (src, dst) in mixes.items():
@@ -206,8 +215,9 @@ def stream_mix_ceilings(zo, torch, state, g, gb, d, mode):
             if rep and (best is None or ms < best):
                 best = ms
         gbs = (len(src) + len(dst)) * 4.0 * d / 1e9 / (best / 1000.0)
-        out[name] = {"reads": len(src), "writes": len(dst), "gbs": round(gbs, 1),
-                     "frac": round(gbs / HBM_PEAK_GBS, 4)}
+        in_place = sum(1 for t in dst if any(t is s for s in src))
+        out[name] = {"reads": len(src), "writes": len(dst), "in_place": in_place,
+                     "gbs": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
     return out
 
 

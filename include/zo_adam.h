@@ -320,11 +320,14 @@ int zo_diag_divsqrt(const float *a, const float *b, float *q, float *r, int64_t 
 int zo_diag_copy(const float *src, float *dst, int64_t n, int nontemporal, hipStream_t stream);
 
 /* dst[w][i] = (sum over r of src[r][i]) + w for i < n: nsrc in [1, 6] read
- * streams and ndst in [1, 4] write streams of float[n] (n a multiple of 4,
+ * streams and ndst in [1, 5] write streams of float[n] (n a multiple of 4,
  * 16-byte aligned device buffers; src and dst are host arrays of device
- * pointers; a dst buffer must not be a src buffer), one float4 per thread
- * with nontemporal accesses like the streaming kernels.  Timing it measures
- * the HBM rate reachable by a kernel with the same mix of arrays. */
+ * pointers), one float4 per thread with nontemporal accesses like the
+ * streaming kernels.  A dst may be one of the srcs (the array is then read
+ * and rewritten in place: each thread stores after all of its loads, and the
+ * sum uses the old values); two dsts may not be the same buffer (ZO_EINVAL),
+ * and buffers may not otherwise overlap.  Timing it measures the HBM rate
+ * reachable by a kernel with the same mix of arrays. */
 int zo_diag_stream(const float *const *src, int32_t nsrc, float *const *dst, int32_t ndst,
                    int64_t n, hipStream_t stream);
 

@@ -615,7 +615,7 @@ int zo_diag_copy(const float *src, float *dst, int64_t n, int nontemporal, hipSt
 int zo_diag_stream(const float *const *src, int32_t nsrc, float *const *dst, int32_t ndst,
                    int64_t n, hipStream_t stream)
 {
-    if (nsrc < 1 || nsrc > 6 || ndst < 1 || ndst > 4 || !src || !dst) return ZO_EINVAL;
+    if (nsrc < 1 || nsrc > 6 || ndst < 1 || ndst > 5 || !src || !dst) return ZO_EINVAL;
     if (n < 0 || n % 4) return ZO_EINVAL;
     zo::StreamPtrs p{};
     for (int32_t r = 0; r < nsrc; ++r) {
@@ -626,6 +626,8 @@ int zo_diag_stream(const float *const *src, int32_t nsrc, float *const *dst, int
     for (int32_t w = 0; w < ndst; ++w) {
         if (n > 0 && !dst[w]) return ZO_EINVAL;
         if (!aligned(dst[w], 16)) return ZO_EALIGN;
+        for (int32_t k = 0; k < w; ++k)
+            if (n > 0 && dst[k] == dst[w]) return ZO_EINVAL;  // one writer per array
         p.dst[w] = dst[w];
     }
     hipError_t e = zo::launch_stream(nsrc, ndst, p, n, stream);

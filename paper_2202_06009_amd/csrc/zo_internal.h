@@ -105,7 +105,7 @@ hipError_t launch_copy(const float *src, float *dst, int64_t n, bool nt, hipStre
 // Streams of the HBM-mix diagnostic: up to 6 read and 4 write arrays.
 struct StreamPtrs {
     const float *src[6];
-    float *dst[4];
+    float *dst[5];
 };
 hipError_t launch_stream(int R, int S, const StreamPtrs &p, int64_t n, hipStream_t st);
 hipError_t launch_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,

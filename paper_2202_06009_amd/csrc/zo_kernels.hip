@@ -985,7 +985,9 @@ __global__ __launch_bounds__(256) void k_copy(const float *__restrict__ src, flo
 
 // R read streams and S write streams of float4, one float4 per thread per
 // stream, nontemporal: the achievable HBM rate of a streaming kernel's mix of
-// arrays (every write depends on every read, so no load is dead).
+// arrays (every write depends on every read, so no load is dead, and a thread
+// issues its stores after all of its loads: a dst that is also a src is
+// updated in place, like the optimizer states a kernel reads and rewrites).
 template <int R, int S>
 __global__ __launch_bounds__(256) void k_stream(StreamPtrs p, int64_t n4)
 {
@@ -1363,6 +1365,7 @@ static hipError_t stream_r(int S, const StreamPtrs &p, int64_t n4, hipStream_t s
     case 2: hipLaunchKernelGGL((k_stream<R, 2>), grid, block, 0, st, p, n4); break;
     case 3: hipLaunchKernelGGL((k_stream<R, 3>), grid, block, 0, st, p, n4); break;
     case 4: hipLaunchKernelGGL((k_stream<R, 4>), grid, block, 0, st, p, n4); break;
+    case 5: hipLaunchKernelGGL((k_stream<R, 5>), grid, block, 0, st, p, n4); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

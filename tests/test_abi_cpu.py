@@ -126,9 +126,14 @@ def test_diag_stream_validates_before_touching_the_device():
     assert lib.zo_diag_stream(None, 1, None, 1, 16, None) == zo.ZO_EINVAL
     arr = (ctypes.c_void_p * 7)()
     assert lib.zo_diag_stream(arr, 7, arr, 1, 16, None) == zo.ZO_EINVAL   # too many reads
-    assert lib.zo_diag_stream(arr, 1, arr, 5, 16, None) == zo.ZO_EINVAL   # too many writes
+    assert lib.zo_diag_stream(arr, 1, arr, 6, 16, None) == zo.ZO_EINVAL   # too many writes
     assert lib.zo_diag_stream(arr, 1, arr, 1, 6, None) == zo.ZO_EINVAL    # n not a multiple of 4
     assert lib.zo_diag_stream(arr, 1, arr, 1, 16, None) == zo.ZO_EINVAL   # null buffers
+    # two writers of one array (the pointers are never dereferenced: the
+    # call fails validation before anything is launched)
+    src = (ctypes.c_void_p * 1)(0x10000)
+    dst = (ctypes.c_void_p * 2)(0x20000, 0x20000)
+    assert lib.zo_diag_stream(src, 1, dst, 2, 16, None) == zo.ZO_EINVAL
 
 
 def test_unknown_algorithm_is_rejected():

@@ -223,3 +223,12 @@ def test_diag_stream_mix(torch_cuda):
     for w in range(4):
         ref = (acc + np.float32(w)).astype(np.float32)
         assert np.array_equal(dst[w].cpu().numpy(), ref)
+    # in place: sources 1 and 3 are rewritten from the sum of the old values,
+    # next to three write-only arrays
+    dst = [src[1], torch.empty_like(src[0]), src[3], torch.empty_like(src[0]),
+           torch.empty_like(src[0])]
+    zo.zo_diag_stream(src, dst)
+    torch.cuda.synchronize()
+    for w in range(5):
+        ref = (acc + np.float32(w)).astype(np.float32)
+        assert np.array_equal(dst[w].cpu().numpy(), ref), w

@@ -1,7 +1,8 @@
 """Pins of the CPU oracle against what the paper and the mathematics fix.
 
-Each test ties one part of the oracle to something other than itself: a
-worked example derived by hand from Equation 3 and Algorithm 2, closed forms
+Each test ties one part of the oracle to something other than itself:
+worked examples derived by hand from Equation 3 and Algorithm 2 (the
+fixtures under tests/golden, one with a non-dyadic average), closed forms
 and invariants of the compressor (contraction identities, error-feedback
 telescoping), brute-force bit packing, an exact rational average, the
 special case in which 0/1 Adam reduces to Adam (Equation 2, computed by an
@@ -14,6 +15,7 @@ from fractions import Fraction
 import numpy as np
 import pytest
 
+import golden_io
 import oracle as orc
 from oracle.brute_adam import adam_fp64
 
@@ -26,43 +28,49 @@ def rng(seed):
 
 
 # ---------------------------------------------------------------------------
-# Worked example (Equation 3 + Algorithm 2 + the sync lines of Algorithm 1),
-# derived by hand; every number below is exact in binary32.
+# Worked examples (Equation 3 + Algorithm 2 + the sync lines of Algorithm 1),
+# derived by hand: the fixtures under tests/golden, each with its derivation.
 # ---------------------------------------------------------------------------
 
-def test_worked_example_compress_server_sync():
-    lay = orc.Layout.from_lengths([4])
-    a = np.array([3, -1, 0, -4], F32)
-    delta = np.zeros(4, F32)
-    words, scales = orc.ef_compress(lay, a, delta)
-    # |a|_1 by the tree: (3 + 1) + (0 + 4) = 8, s = 8 / 4 = 2
-    assert scales[0] == F32(2.0)
-    # signs +,-,+(zero),-  -> bits 1,0,1,0 LSB first -> 0b0101
-    assert int(words[0]) == 0x5
-    # new error a - s*sign = [1, 1, -2, -2]
-    np.testing.assert_array_equal(delta, np.array([1, 1, -2, -2], F32))
-
-    # server with W = 2: peer signs +,+,-,- (0b0011) with scale 1
-    words_w = np.array([[0x5], [0x3]], np.uint64)
-    scales_w = np.array([[2.0], [1.0]], F32)
-    srv_err = np.zeros(4, F32)
+@pytest.mark.parametrize("name", golden_io.names())
+def test_worked_examples(name):
+    """The hand-derived examples of tests/golden (Equation 3, Algorithm 2,
+    Algorithm 1's sync lines), part by part and as one step from g."""
+    su, ex = golden_io.load(name)
+    lay = orc.Layout.from_segments(su["segments"], su["chunk"])
+    assert lay.nchunks == 1
+    eq = np.testing.assert_array_equal
+    # worker compress on a with zero error
+    delta = np.zeros(lay.n, F32)
+    words, scales = orc.ef_compress(lay, ex["a"], delta)
+    eq(words, ex["own_words"])
+    eq(scales, ex["own_scales"])
+    eq(delta, ex["err"])
+    # server over [own, peers]
+    words_w = np.concatenate([words[None, :], su["peer_words"][:, None]], axis=0)
+    scales_w = np.concatenate([scales[None, :], su["peer_scales"][:, None]], axis=0)
+    assert words_w.shape[0] == su["world"]
+    srv_err = np.zeros(lay.n, F32)
     sw, ss, avg = orc.server(lay, words_w, scales_w, srv_err, want_avg=True)
-    # ([2,-2,2,-2] + [1,1,-1,-1]) / 2
-    np.testing.assert_array_equal(avg, np.array([1.5, -0.5, 0.5, -1.5], F32))
-    # tree (1.5 + 0.5) + (0.5 + 1.5) = 4, s = 1; signs +,-,+,- -> 0b0101
-    assert ss[0] == F32(1.0) and int(sw[0]) == 0x5
-    np.testing.assert_array_equal(srv_err, np.array([0.5, 0.5, -0.5, -0.5], F32))
-    ubar = orc.decompress(lay, sw, ss)
-    np.testing.assert_array_equal(ubar, np.array([1, -1, 1, -1], F32))
-
-    # sync with Gamma = 0.5, v = 4 (sqrt(4 + 1e-8) rounds to 2), anchor = 10
-    w = orc.Worker(lay, np.full(4, 10, F32))
-    w.v[:] = 4.0
-    w.gamma_sum = F32(0.5)
-    w.sync(sw, ss)
-    np.testing.assert_array_equal(w.m, np.array([2, -2, 2, -2], F32))
-    np.testing.assert_array_equal(w.x, np.array([9.5, 10.5, 9.5, 10.5], F32))
-    np.testing.assert_array_equal(w.anchor, w.x)
+    eq(avg, ex["avg"])
+    eq(sw, ex["srv_words"])
+    eq(ss, ex["srv_scales"])
+    eq(srv_err, ex["srv_err"])
+    eq(orc.decompress(lay, sw, ss), ex["ubar"])
+    # the whole step from the gradient
+    w = orc.Worker(lay, su["x0"], beta1=su["beta1"], eps=su["eps"])
+    w.v[:] = su["v0"]
+    out = w.step(su["gamma"], su["g"], sync=True, var=False,
+                 peer_words=su["peer_words"][:, None], peer_scales=su["peer_scales"][:, None])
+    eq(out["own_words"], ex["own_words"])
+    eq(out["srv_words"], ex["srv_words"])
+    eq(out["srv_scales"], ex["srv_scales"])
+    eq(w.err, ex["err"])
+    eq(w.srv_err, ex["srv_err"])
+    eq(w.m, ex["m"])
+    eq(w.x, ex["x"])
+    eq(w.anchor, w.x)
+    eq(w.v, su["v0"])
     assert not w.u.any() and w.gamma_sum == 0
 
 
