@@ -74,6 +74,43 @@ def source_hash():
         return hashlib.sha256(f.read()).hexdigest()
 
 
+def summarize_counters(dirs, mode):
+    """Mean per dispatch of every counter in the rocprofv3 --pmc runs under
+    `dirs`, for each timed kernel of `mode`, as a markdown table, with the
+    ratios that need no unit: instructions per wave, and the share of the
+    LDS's active cycles lost to bank conflicts."""
+    keys = kernel_keys(mode)
+    vals = {}
+    for d in dirs:
+        for root, _, files in os.walk(d):
+            for fn in files:
+                if not fn.endswith("counter_collection.csv"):
+                    continue
+                for r in csv.DictReader(open(os.path.join(root, fn))):
+                    name = r["Kernel_Name"].replace("void ", "")
+                    for pattern, (key, kind) in keys.items():
+                        if kind is not None and re.match(pattern, name):
+                            vals.setdefault(key, {}).setdefault(r["Counter_Name"], []).append(
+                                float(r["Counter_Value"]))
+    names = [k for _, (k, kind) in keys.items() if kind is not None and k in vals]
+    mean = {k: {c: sum(v) / len(v) for c, v in vals[k].items()} for k in names}
+    counters = sorted({c for k in names for c in mean[k]})
+    print("| counter | " + " | ".join(names) + " |")
+    print("|---|" + "---|" * len(names))
+    for c in counters:
+        print(f"| {c} | " + " | ".join(f"{mean[k].get(c, float('nan')):.4g}" for k in names) + " |")
+    def ratio(k, a, b):
+        m = mean[k]
+        return f"{m[a] / m[b]:.3g}" if a in m and b in m and m[b] else "-"
+    for label, a, b in (("VALU instructions per wave", "SQ_INSTS_VALU", "SQ_WAVES"),
+                        ("LDS instructions per wave", "SQ_INSTS_LDS", "SQ_WAVES"),
+                        ("SALU instructions per wave", "SQ_INSTS_SALU", "SQ_WAVES"),
+                        ("vector memory reads per wave", "SQ_INSTS_VMEM_RD", "SQ_WAVES"),
+                        ("LDS bank-conflict cycles / LDS active cycles", "SQ_LDS_BANK_CONFLICT",
+                         "SQ_LDS_IDX_ACTIVE")):
+        print(f"| {label} | " + " | ".join(ratio(k, a, b) for k in names) + " |")
+
+
 def summarize_pmc(fetch_dir, write_dir, out_path, mode):
     """Turn two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over
     `bench.py --copy-calibration` into per-launch HBM traffic, each counter
@@ -283,6 +320,8 @@ def main():
                     help="first run plain and nontemporal copies of a known size (for counters)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="PMC_DIR",
+                    help="print the timed kernels' counters from rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
     fv = args.algorithm == "frozen-variance"
     mode = "frozen-variance" if fv else ("eager" if args.eager_sync_writes else "deferred")
@@ -290,6 +329,9 @@ def main():
         mode += f"/{args.grad_dtype}"
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], TRAFFIC_FILE, mode)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, mode)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the multi-GPU exchange of the method is not "
