@@ -258,6 +258,51 @@ def stream_mix_ceilings(zo, torch, state, g, gb, d, mode):
     return out
 
 
+def server_share(zo, torch, wl, state, g_in, packed, scales, srv_packed, srv_scales, W, reps=10):
+    """The server at its per-GPU shape under the sharded design: GPU k = W/2
+    serves a chunk-aligned range of about d/W elements, whose W-slot input
+    holds every worker's words and scales for that range only (what the
+    all-to-all delivers).  Each rep is a full sync step on a handle whose
+    server range is that share (compress and reconstruct over all d, as every
+    GPU runs them); the server launch is timed with HIP events.  Inputs are
+    the bench's buffers (the slot of the range's own words is synthetic)."""
+    start, ln, word, nwords = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
+    nch, d = len(ln), wl.n
+    k = W // 2
+    c0 = next(c for c in range(nch) if start[c] >= k * d // W)
+    c1 = next((c for c in range(c0, nch) if start[c] >= (k + 1) * d // W), nch)
+    w0, w1 = int(word[c0]), int(word[c1] if c1 < nch else nwords)
+    ne = int(start[c1 - 1] + ln[c1 - 1] - start[c0])
+    rp = packed[:, w0:w1].contiguous()
+    rs = scales[:, c0:c1].contiguous()
+    opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=W, chunk=wl.chunk,
+                    seg_off=wl.seg_off, tv=[], tu=list(range(reps)), state=state,
+                    srv_chunk_begin=c0, srv_chunk_end=c1, defer_sync_writes=True,
+                    grad_dtype="f32" if g_in.dtype == torch.float32 else
+                    ("bf16" if g_in.dtype == torch.bfloat16 else "f16"))
+    ms = []
+    try:
+        for t in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            opt.compress_pack_ef(t, 1e-4, g_in, packed[0], scales[0])
+            e0.record()
+            opt.unpack_average(t, rp, rs, srv_packed, srv_scales)
+            e1.record()
+            opt.sync_update(t, srv_packed, srv_scales, None)
+            torch.cuda.synchronize()
+            if t >= 2:
+                ms.append(e0.elapsed_time(e1))
+    finally:
+        opt.close()
+    avg = sum(ms) / len(ms)
+    pk, sc = 8 * (w1 - w0), 4 * (c1 - c0)
+    nbytes = W * (pk + sc) + 8 * ne + pk + sc
+    return {"gpu": k, "chunks": [c0, c1], "params": ne, "ms": round(avg, 4),
+            "gb_per_launch": round(nbytes / 1e9, 4),
+            "gbs": round(nbytes / 1e9 / (avg / 1000.0), 1),
+            "frac": round(nbytes / 1e9 / (avg / 1000.0) / HBM_PEAK_GBS, 4)}
+
+
 def cpu_baseline(wl, sample_chunks, fv=False):
     """Time the oracle on the first `sample_chunks` chunks of the shard: one
     local step with variance update and one sync step with variance update
@@ -436,6 +481,8 @@ def main():
                   / args.steps for i, n in enumerate(names)}
     inexact = opt.inexact_chunks()
     opt.close()
+    share = None if fv else server_share(zo, torch, wl, state, g_in, packed, scales, srv_packed,
+                                         srv_scales, W)
     # (the diagnostic streams binary32 arrays: no like-for-like mix for 16-bit gradients)
     mix = stream_mix_ceilings(zo, torch, state, g, gb, d, mode) \
         if args.grad_dtype == "f32" else None
@@ -482,6 +529,12 @@ def main():
         "kernels": kernels,
         "inexact_chunks": inexact,
         "stream_mix_ceiling": mix,
+        # the server at one GPU's share of a W-GPU sharded run, and that GPU's time for a
+        # local+variance and a sync+variance step there, collectives excluded
+        "server_share": share,
+        "sharded_ms_per_step_no_collectives": None if share is None else round(
+            per_kernel["local+var"] + per_kernel["sync1"] + share["ms"] + per_kernel["recon+var"],
+            4),
         "roofline": {"bound": "hbm", "kernel": dom,
                      "achieved": kernels[dom]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": kernels[dom]["frac"], "traffic": traffic_gb},
