@@ -145,10 +145,12 @@ __device__ __forceinline__ bool chunk_slot(Chunks ch, int64_t nchunks, int bpc, 
 __device__ __forceinline__ f4v m_from_copy(const SrvCopy &sm, const Chunks &ch, int64_t c, int e)
 {
     const uint32_t bits = sm.words32[2 * ch.word[c] + (e >> 5)] >> (e & 31);
-    const float sc = sm.scales[c];
+    // (-S)/Gamma = -(S/Gamma): a rounded quotient is odd in its dividend, so
+    // one division per chunk gives every element's value
+    const float mq = sm.scales[c] / sm.gamma_m;
     f4v r;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) r[q] = (((bits >> q) & 1u) ? sc : -sc) / sm.gamma_m;
+    for (int q = 0; q < 4; ++q) r[q] = ((bits >> q) & 1u) ? mq : -mq;
     return r;
 }
 
@@ -862,10 +864,11 @@ __global__ __launch_bounds__(256) void k_recon(const uint32_t *__restrict__ srv_
     f4v gb;
     if (VAR) gb = ldg4<GT>(gbar, i4);
     f4v mm, xx, nv;
+    const float mq = sc / gsum;  // odd in sc, so one division serves both signs
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         const float ub = ((bits >> q) & 1u) ? sc : -sc;
-        mm[q] = ub / gsum;
+        mm[q] = ((bits >> q) & 1u) ? mq : -mq;
         xx[q] = an[q] - ub / sqrtf(vv[q] + s.eps);
         if (VAR) nv[q] = var_elem(vv[q], gb[q], s);
     }
