@@ -20,8 +20,11 @@
  *   - Every call validates all of its arguments on the host before enqueueing
  *     anything; a rejected call returns a negative status and changes nothing.
  *   - Calls are asynchronous on the stream given to zo_adam_init (or
- *     zo_set_stream): they return after enqueueing one kernel.  Device faults
- *     surface at the caller's synchronisation.
+ *     zo_set_stream): each hot-path call (zo_local_step, zo_compress_pack_ef,
+ *     zo_unpack_average, zo_sync_update, zo_variance_update,
+ *     zo_fullprec_step) returns after enqueueing one kernel; zo_read_state
+ *     enqueues one and zo_materialize up to three elementwise kernels.
+ *     Device faults surface at the caller's synchronisation.
  *   - No entry point after zo_adam_init allocates memory.
  *   - A handle is not thread-safe; use one handle per stream.
  *   - Arithmetic is IEEE binary32 with one rounding per operation, no FMA
@@ -155,13 +158,15 @@ typedef struct zo_state {
 /*
  * zo_adam_init -- set up the handle (Algorithm 1, its "Require" line).
  * Validates the configuration, builds the chunk table and copies it to the
- * device (the only allocations the library makes), then enqueues on `stream`:
+ * device, and allocates one flag byte per server chunk and, with
+ * defer_sync_writes, the copy of the server's packed words and scales (the
+ * only device allocations the library makes), then enqueues on `stream`:
  * m = v = u = err = srv_err = 0 and anchor = x.  Gamma = 0, next step t = 0.
  * Returns ZO_OK and *h, or an error (then *h is NULL).
  */
 int zo_adam_init(zo_adam **h, const zo_config *cfg, const zo_state *st, hipStream_t stream);
 
-/* Release the handle and its device chunk table.  Waits for the stream. */
+/* Release the handle and its device memory.  Waits for the stream. */
 int zo_adam_destroy(zo_adam *h);
 
 /* Change the stream later calls enqueue on. */
@@ -248,7 +253,8 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
 
 /*
  * zo_fullprec_step -- ZO_ALG_FROZEN_VARIANCE, t in T_v: one step of
- * Algorithm 4 with the full-precision AllReduce output gbar (device float[n]):
+ * Algorithm 4 with the full-precision AllReduce output gbar (device [n] of
+ * grad_dtype):
  *   v <- beta2 v + (1 - beta2) gbar^2;  m <- beta1 m + (1 - beta1) gbar;
  *   x <- x - gamma m_t / sqrt(v_t + eps)   (m_t, v_t from before the step).
  * ZO_EINVAL on a ZO_ALG_ZERO_ONE_ADAM handle; ZO_ESTATE if t is not the next
@@ -259,7 +265,8 @@ int zo_fullprec_step(zo_adam *h, int64_t t, float gamma, const void *gbar);
 /*
  * zo_variance_update -- the variance line of Algorithm 1 for t in T_v when it
  * was not fused: v <- beta2 v + (1 - beta2) gbar^2, after the other calls of
- * step t.  gbar: device float[n], the full-precision AllReduce output.
+ * step t.  gbar: device [n] of grad_dtype, the full-precision AllReduce
+ * output.
  */
 int zo_variance_update(zo_adam *h, int64_t t, const void *gbar);
 
