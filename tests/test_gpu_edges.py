@@ -1,6 +1,6 @@
-"""GPU edge cases: call order, argument errors, an empty shard, the server
-restricted to a chunk range, pad bits on input, the exact-sum condition,
-run-to-run determinism."""
+"""GPU edge cases: call order, argument errors, an empty shard, a shard of
+more than 2^31 parameters, the server restricted to a chunk range, pad bits on
+input, the exact-sum condition, run-to-run determinism."""
 import numpy as np
 import pytest
 
@@ -83,6 +83,36 @@ def test_empty_shard(torch_cuda):
         assert run.opt.next_step == 3
     finally:
         run.close()
+
+
+@pytest.mark.timeout(600)
+def test_shard_beyond_2_31_elements(torch_cuda):
+    """2,167,001,004 parameters in three segments, so element indices, packed
+    bit indices and float4 indices pass 2^31 (the 64-bit index arithmetic of
+    every kernel), in the benchmark's alternation of a local and a sync step
+    with the variance update and deferred sync writes, W = 4.  Sampled: both
+    ends of every segment, a stride, the chunks around element 2^31 and the
+    ragged last chunk; every state and packed output after every step."""
+    import harness
+    import oracle as orc
+    T = 4
+    wl = C.Workload(name="beyond-2^31", seg_off=C.offsets([1_500_000_000, 667_000_004, 1000]),
+                    world=4, chunk=16384, steps=T, tv=list(range(T)), tu=[1, 3],
+                    gammas=[1e-4] * T, sigma_g=1e-3)
+    assert wl.n > 2 ** 31
+    lay = orc.Layout.from_segments(wl.seg_off, wl.chunk)
+    ids = set(harness.sample_chunks(lay, wl.seg_off, 100000, 20000).tolist())
+    b = int(np.searchsorted(lay.cstart, 2 ** 31, side="right")) - 1  # holds element 2^31
+    ids.update(range(b - 2, min(b + 3, lay.nchunks)))
+    ids.add(lay.nchunks - 1)
+    ids = np.array(sorted(ids), dtype=np.int64)
+    print(f"{wl.name}: d={wl.n}, {len(ids)} chunks sampled (chunk {b} holds element 2^31)",
+          flush=True)
+    report, inexact = harness.run_parity(wl, chunk_ids=ids, log=lambda m: print(m, flush=True),
+                                         defer=True)
+    for t, bad in enumerate(report):
+        assert not bad, f"mismatch after step {t - 1}: {bad}"
+    assert inexact == 0
 
 
 def test_server_range_matches_single_server(torch_cuda):
