@@ -3,7 +3,7 @@
 // Validates every call before launching anything, keeps the step state
 // machine of Algorithm 1 (which lines of step t have run), accumulates the
 // learning-rate sum Gamma of the current interval in binary32, and launches
-// exactly one kernel per call on the handle's stream.
+// exactly one kernel per hot-path call on the handle's stream.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
