@@ -303,6 +303,46 @@ def server_share(zo, torch, wl, state, g_in, packed, scales, srv_packed, srv_sca
             "frac": round(nbytes / 1e9 / (avg / 1000.0) / HBM_PEAK_GBS, 4)}
 
 
+def schedule_run(zo, torch, wl, state, g_in, gb_in, packed, scales, srv_packed, srv_scales,
+                 deferred, grad_dtype):
+    """The workload's own schedule once (its T_v and T_u over its steps, its
+    learning rates): sync steps while the variance is updated, then local
+    steps between ever rarer syncs.  Timed with HIP events around the whole
+    run (after one untimed run of the same schedule on another handle);
+    run-level params/s = d * steps / time.  Inputs are the bench's buffers,
+    reused at every step."""
+    tu, tv = set(wl.tu), set(wl.tv)
+
+    def run(timed):
+        opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=wl.world,
+                        chunk=wl.chunk, seg_off=wl.seg_off, tv=wl.tv, tu=wl.tu, state=state,
+                        defer_sync_writes=deferred, grad_dtype=grad_dtype)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        try:
+            torch.cuda.synchronize()
+            e0.record()
+            for t in range(wl.steps):
+                gam, gb = wl.gamma(t), (gb_in if t in tv else None)
+                if t in tu:
+                    opt.compress_pack_ef(t, gam, g_in, packed[0], scales[0])
+                    opt.unpack_average(t, packed, scales, srv_packed, srv_scales)
+                    opt.sync_update(t, srv_packed, srv_scales, gb)
+                else:
+                    opt.local_step(t, gam, g_in, gb)
+            e1.record()
+            torch.cuda.synchronize()
+        finally:
+            opt.close()
+        return e0.elapsed_time(e1)
+
+    run(False)
+    ms = run(True)
+    return {"steps": wl.steps, "syncs": len(tu), "variance_updates": len(tv),
+            "local_steps": wl.steps - len(tu), "ms": round(ms, 3),
+            "ms_per_step": round(ms / wl.steps, 4),
+            "params_per_s": round(wl.n * wl.steps / (ms / 1000.0), 1)}
+
+
 def cpu_baseline(wl, sample_chunks, fv=False):
     """Time the oracle on the first `sample_chunks` chunks of the shard: one
     local step with variance update and one sync step with variance update
@@ -332,18 +372,32 @@ def cpu_baseline(wl, sample_chunks, fv=False):
         worker = orc.FVWorker(lay, x0, wl.beta1, wl.beta2, wl.eps)
         t0 = time.perf_counter()
         worker.step(np.float32(1e-4), g, True, gbar=gb)
+        t1 = time.perf_counter()
         worker.step(np.float32(1e-4), g, False, peer_words=pw, peer_scales=ps)
         what = "one full-precision and one compressed step of Algorithm 4"
+        kinds = ("full-precision", "compressed")
     else:
         worker = orc.Worker(lay, x0, wl.beta1, wl.beta2, wl.eps)
         t0 = time.perf_counter()
         worker.step(np.float32(1e-4), g, False, True, gbar=gb)
+        t1 = time.perf_counter()
         worker.step(np.float32(1e-4), g, True, True, gbar=gb, peer_words=pw, peer_scales=ps)
         what = "one local+variance step and one sync+variance step"
-    dt = time.perf_counter() - t0
+        kinds = ("local+var", "sync+var")
+    t2 = time.perf_counter()
+    dt = t2 - t0
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
     return {"value": 2 * n / dt, "unit": "params/s", "cores": 1, "kind": "oracle",
             "sample": f"first {nch} chunks ({n} params) of the same shard, W={W}: {what}, "
-                      f"{dt:.2f} s"}
+                      f"{dt:.2f} s",
+            "ns_per_param": {kinds[0]: round((t1 - t0) * 1e9 / n, 2),
+                             kinds[1]: round((t2 - t1) * 1e9 / n, 2)},
+            "cpu": model}
 
 
 def main():
@@ -352,7 +406,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="gpt2-1.5b")
-    ap.add_argument("--cpu-sample-chunks", type=int, default=1600)
+    ap.add_argument("--cpu-sample-chunks", type=int, default=2048,
+                    help="chunks of the shard the CPU oracle is timed on (GPT-2: 33.5M params)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--eager-sync-writes", action="store_true",
                     help="the reconstruction writes x and u at every sync")
@@ -477,12 +532,28 @@ def main():
         bench_step(args.warmup + k, evs[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per_kernel = {n: sum(evs[k][i][0].elapsed_time(evs[k][i][1]) for k in range(args.steps))
-                  / args.steps for i, n in enumerate(names)}
+    times = {n: sorted(evs[k][i][0].elapsed_time(evs[k][i][1]) for k in range(args.steps))
+             for i, n in enumerate(names)}
+    per_kernel = {n: sum(v) / len(v) for n, v in times.items()}
+    median = {n: (v[(len(v) - 1) // 2] + v[len(v) // 2]) / 2 for n, v in times.items()}
     inexact = opt.inexact_chunks()
     opt.close()
     share = None if fv else server_share(zo, torch, wl, state, g_in, packed, scales, srv_packed,
                                          srv_scales, W)
+    sched = None if fv else schedule_run(zo, torch, wl, state, g_in, gb_in, packed, scales,
+                                         srv_packed, srv_scales, not args.eager_sync_writes,
+                                         args.grad_dtype)
+    # the practical ceiling: a plain copy of one state vector (best of three)
+    copy_ms = []
+    for _ in range(3):
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record()
+        zo.zo_diag_copy(state["x"], state["m"], nontemporal=True)
+        c1.record()
+        torch.cuda.synchronize()
+        copy_ms.append(c0.elapsed_time(c1))
+    copy_gbs = 8.0 * d / 1e9 / (min(copy_ms) / 1000.0)
+    props = torch.cuda.get_device_properties(dev)
     # (the diagnostic streams binary32 arrays: no like-for-like mix for 16-bit gradients)
     mix = stream_mix_ceilings(zo, torch, state, g, gb, d, mode) \
         if args.grad_dtype == "f32" else None
@@ -493,9 +564,13 @@ def main():
         algorithmic_bytes(d, nchunks, nwords, W, deferred=not args.eager_sync_writes,
                           gbytes=gbytes)
     kernels = {n: {"ms": round(per_kernel[n], 4),
+                   "ms_median": round(median[n], 4),
+                   "params_per_s": round(d / (per_kernel[n] / 1000.0), 1),
                    "gb_per_launch": round(bytes_[n] / 1e9, 3),
                    "gbs": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0), 1),
-                   "frac": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0) / HBM_PEAK_GBS, 4)}
+                   "frac": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0) / HBM_PEAK_GBS, 4),
+                   "frac_of_copy": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0) / copy_gbs,
+                                         4)}
                for n in names}
     dom = max(names, key=lambda n: per_kernel[n])
     step_bytes = sum(bytes_.values())
@@ -528,13 +603,19 @@ def main():
         "hbm_frac_step": round(step_bytes / 1e9 / (ms_per_step / 1000.0) / HBM_PEAK_GBS, 4),
         "kernels": kernels,
         "inexact_chunks": inexact,
+        "copy_gbs": round(copy_gbs, 1),
         "stream_mix_ceiling": mix,
+        # the workload's own schedule once (mostly local steps after the warm-up phase)
+        "schedule_run": sched,
         # the server at one GPU's share of a W-GPU sharded run, and that GPU's time for a
         # local+variance and a sync+variance step there, collectives excluded
         "server_share": share,
         "sharded_ms_per_step_no_collectives": None if share is None else round(
             per_kernel["local+var"] + per_kernel["sync1"] + share["ms"] + per_kernel["recon+var"],
             4),
+        "env": {"device": props.name, "arch": getattr(props, "gcnArchName", None),
+                "compute_units": props.multi_processor_count, "hip": torch.version.hip,
+                "torch": torch.__version__},
         "roofline": {"bound": "hbm", "kernel": dom,
                      "achieved": kernels[dom]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": kernels[dom]["frac"], "traffic": traffic_gb},
