@@ -111,6 +111,50 @@ def summarize_counters(dirs, mode):
         print(f"| {label} | " + " | ".join(ratio(k, a, b) for k in names) + " |")
 
 
+def summarize_trace(trace_dir, mode, workload, warmup, steps):
+    """Per-kernel durations of a `rocprofv3 --kernel-trace` run of this bench
+    (the default command: `warmup` + `steps` bench steps) over the timed
+    dispatches only: for each of the step's four kernel slots (all template
+    variants of the slot's kernel, in launch order), dispatches warmup ..
+    warmup + steps - 1.  Later launches of the same kernels (the server share
+    and the schedule run after the timed region) are left out.  Prints a
+    markdown table with the algorithmic bytes of the workload."""
+    import statistics
+    import paper_2202_06009_amd as zo
+    from synth import configs as C
+    base, _, dt = mode.partition("/")
+    fv = base == "frozen-variance"
+    slots = ([("fv_full", r"zo::k_fv_full<"), ("sync1", r"zo::k_sync1<"),
+              ("srv", r"zo::k_srv_(lut|plain)<"), ("fv_apply", r"zo::k_fv_apply")] if fv else
+             [("local+var", r"zo::k_local<"), ("sync1", r"zo::k_sync1<"),
+              ("srv", r"zo::k_srv_(lut|plain)<"), ("recon+var", r"zo::k_recon<")])
+    rows = []
+    for root, _, files in os.walk(trace_dir):
+        for fn in files:
+            if fn.endswith("kernel_trace.csv"):
+                rows += list(csv.DictReader(open(os.path.join(root, fn))))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    wl = C.get(workload)
+    _, ln, _, nwords = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
+    gbytes = {"": 4, "f16": 2, "bf16": 2}[dt]
+    model = algorithmic_bytes_fv(wl.n, len(ln), nwords, wl.world, gbytes) if fv else \
+        algorithmic_bytes(wl.n, len(ln), nwords, wl.world, deferred=base == "deferred",
+                          gbytes=gbytes)
+    print("| kernel | calls | avg µs | median µs | min µs | max µs | algorithmic GB/launch "
+          "| GB/s | % of 8 TB/s |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for key, pat in slots:
+        ds = [r for r in rows if re.match(pat, r["Kernel_Name"].replace("void ", ""))]
+        ds = ds[warmup:warmup + steps]
+        us = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0 for r in ds]
+        names = sorted({r["Kernel_Name"].replace("void ", "").split("(")[0] for r in ds})
+        avg = sum(us) / len(us)
+        gbs = model[key] / 1e9 / (avg / 1e6)
+        print(f"| `{', '.join(names)}` ({key}) | {len(us)} | {avg:.1f} | "
+              f"{statistics.median(us):.1f} | {min(us):.1f} | {max(us):.1f} | "
+              f"{model[key] / 1e9:.3f} | {gbs:.0f} | {100 * gbs / HBM_PEAK_GBS:.1f} |")
+
+
 def summarize_pmc(fetch_dir, write_dir, out_path, mode):
     """Turn two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over
     `bench.py --copy-calibration` into per-launch HBM traffic, each counter
@@ -417,9 +461,13 @@ def main():
                     help="frozen-variance: Algorithm 4 (1-bit Adam's compression stage), one "
                          "full-precision and one compressed step per bench step")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="first run plain and nontemporal copies of a known size (for counters)")
+                    help="counter-collection run: first run plain and nontemporal copies of a "
+                         "known size, and skip the measurements after the timed region")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM traffic summary from two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
+                    help="print the timed kernels' durations from a rocprofv3 --kernel-trace "
+                         "run of this command (same --workload/--warmup/--steps) and exit")
     ap.add_argument("--summarize-counters", nargs="+", metavar="PMC_DIR",
                     help="print the timed kernels' counters from rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
@@ -432,6 +480,9 @@ def main():
         return
     if args.summarize_counters:
         summarize_counters(args.summarize_counters, mode)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, mode, args.workload, args.warmup, args.steps)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the multi-GPU exchange of the method is not "
@@ -538,25 +589,34 @@ def main():
     median = {n: (v[(len(v) - 1) // 2] + v[len(v) // 2]) / 2 for n, v in times.items()}
     inexact = opt.inexact_chunks()
     opt.close()
-    share = None if fv else server_share(zo, torch, wl, state, g_in, packed, scales, srv_packed,
-                                         srv_scales, W)
-    sched = None if fv else schedule_run(zo, torch, wl, state, g_in, gb_in, packed, scales,
-                                         srv_packed, srv_scales, not args.eager_sync_writes,
-                                         args.grad_dtype)
-    # the practical ceiling: a plain copy of one state vector (best of three)
-    copy_ms = []
-    for _ in range(3):
-        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        c0.record()
-        zo.zo_diag_copy(state["x"], state["m"], nontemporal=True)
-        c1.record()
-        torch.cuda.synchronize()
-        copy_ms.append(c0.elapsed_time(c1))
-    copy_gbs = 8.0 * d / 1e9 / (min(copy_ms) / 1000.0)
     props = torch.cuda.get_device_properties(dev)
-    # (the diagnostic streams binary32 arrays: no like-for-like mix for 16-bit gradients)
-    mix = stream_mix_ceilings(zo, torch, state, g, gb, d, mode) \
-        if args.grad_dtype == "f32" else None
+    # Measurements after the timed region.  A counter-collection run
+    # (--copy-calibration) skips them: its counters must come from the timed
+    # kernels and the calibration copies only (the server share and the
+    # schedule run launch the same kernels at other sizes, the ceiling the
+    # same copy kernel).
+    extras = not args.copy_calibration
+    share = sched = mix = None
+    copy_gbs = float("nan")
+    if extras and not fv:
+        share = server_share(zo, torch, wl, state, g_in, packed, scales, srv_packed, srv_scales,
+                             W)
+        sched = schedule_run(zo, torch, wl, state, g_in, gb_in, packed, scales, srv_packed,
+                             srv_scales, not args.eager_sync_writes, args.grad_dtype)
+    if extras:
+        # the practical ceiling: a plain copy of one state vector (best of three)
+        copy_ms = []
+        for _ in range(3):
+            c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            c0.record()
+            zo.zo_diag_copy(state["x"], state["m"], nontemporal=True)
+            c1.record()
+            torch.cuda.synchronize()
+            copy_ms.append(c0.elapsed_time(c1))
+        copy_gbs = 8.0 * d / 1e9 / (min(copy_ms) / 1000.0)
+        # (the diagnostic streams binary32 arrays: no like-for-like mix for 16-bit gradients)
+        if args.grad_dtype == "f32":
+            mix = stream_mix_ceilings(zo, torch, state, g, gb, d, mode)
 
     ms_per_step = wall * 1000.0 / args.steps
     value = 2.0 * d / (ms_per_step / 1000.0)
@@ -569,8 +629,8 @@ def main():
                    "gb_per_launch": round(bytes_[n] / 1e9, 3),
                    "gbs": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0), 1),
                    "frac": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0) / HBM_PEAK_GBS, 4),
-                   "frac_of_copy": round(bytes_[n] / 1e9 / (per_kernel[n] / 1000.0) / copy_gbs,
-                                         4)}
+                   "frac_of_copy": None if not extras else round(
+                       bytes_[n] / 1e9 / (per_kernel[n] / 1000.0) / copy_gbs, 4)}
                for n in names}
     dom = max(names, key=lambda n: per_kernel[n])
     step_bytes = sum(bytes_.values())
@@ -603,7 +663,7 @@ def main():
         "hbm_frac_step": round(step_bytes / 1e9 / (ms_per_step / 1000.0) / HBM_PEAK_GBS, 4),
         "kernels": kernels,
         "inexact_chunks": inexact,
-        "copy_gbs": round(copy_gbs, 1),
+        "copy_gbs": round(copy_gbs, 1) if extras else None,
         "stream_mix_ceiling": mix,
         # the workload's own schedule once (mostly local steps after the warm-up phase)
         "schedule_run": sched,
