@@ -1,0 +1,83 @@
+"""Host-side pieces of bench.py: the algorithmic byte model and the selection
+of the timed dispatches from a kernel trace (no GPU)."""
+import csv
+import os
+
+import pytest
+
+import bench
+
+
+def test_byte_model_per_parameter():
+    """Each kernel's bytes per launch are its arrays' reads and writes, plus
+    packed words (d/8 bytes) and one binary32 scale per chunk."""
+    d, nch, nw, W = 1 << 20, 256, (1 << 20) // 64, 128
+    pk, sc = 8 * nw, 4 * nch
+    deferred = bench.algorithmic_bytes(d, nch, nw, W, deferred=True, gbytes=4)
+    assert deferred["local+var"] == 28 * d + pk + sc       # g, gbar, anchor, v; m, x, v
+    assert deferred["sync1"] == 16 * d + pk + sc           # g, m, err; err
+    assert deferred["srv"] == W * (pk + sc) + 8 * d + pk + sc
+    assert deferred["recon+var"] == 2 * (pk + sc) + 20 * d  # anchor, v, gbar; anchor, v
+    eager = bench.algorithmic_bytes(d, nch, nw, W, deferred=False, gbytes=4)
+    assert eager["local+var"] == 40 * d
+    assert eager["sync1"] == 20 * d + pk + sc
+    assert eager["recon+var"] == pk + sc + 32 * d
+    half = bench.algorithmic_bytes(d, nch, nw, W, deferred=True, gbytes=2)
+    assert deferred["local+var"] - half["local+var"] == 4 * d  # g and gbar in 16 bits
+    fv = bench.algorithmic_bytes_fv(d, nch, nw, W, 4)
+    assert fv["fv_full"] == 28 * d and fv["fv_apply"] == 20 * d + pk + sc
+
+
+def test_gpt2_bytes_per_launch():
+    """The GPT-2-1.5B shard's per-launch figures quoted with the benchmark."""
+    import paper_2202_06009_amd as zo
+    from synth import configs as C
+    wl = C.get("gpt2-1.5b")
+    _, ln, _, nw = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
+    b = bench.algorithmic_bytes(wl.n, len(ln), nw, wl.world, deferred=True)
+    assert round(b["local+var"] / 1e9, 3) == 43.808
+    assert round(b["sync1"] / 1e9, 3) == 25.117
+    assert round(b["srv"] / 1e9, 3) == 37.627
+    assert round(b["recon+var"] / 1e9, 3) == 31.542
+
+
+def _write_trace(path, launches):
+    cols = ["Kind", "Kernel_Name", "Start_Timestamp", "End_Timestamp"]
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=cols)
+        w.writeheader()
+        for name, start, dur in launches:
+            w.writerow({"Kind": "KERNEL_DISPATCH", "Kernel_Name": f"void {name}(int)",
+                        "Start_Timestamp": start, "End_Timestamp": start + dur})
+
+
+def test_trace_summary_keeps_the_timed_dispatches(tmp_path, capsys):
+    """Two warmup and three timed bench steps, then later launches of the same
+    kernels at other sizes: only dispatches 2..4 of each slot count, whatever
+    the template variant."""
+    launches, t = [], 0
+    for step in range(5):
+        for name, dur in ((("zo::k_local<true, 0, true, 0>" if step == 0 else
+                            "zo::k_local<true, 1, false, 0>"), 7000),
+                          ("zo::k_sync1<1024, 4, true, 2, 0>", 4000),
+                          ("zo::k_srv_lut<512, 16>", 7500 + 10 * step),
+                          ("zo::k_recon<true, true, 0>", 5000)):
+            launches.append((name, t, 1000 * dur))
+            t += 10 ** 7
+    for _ in range(4):  # the server share: the same kernels, much shorter
+        for name in ("zo::k_sync1<1024, 4, true, 2, 0>", "zo::k_srv_lut<512, 16>",
+                     "zo::k_recon<true, true, 0>"):
+            launches.append((name, t, 1000 * 80))
+            t += 10 ** 6
+    _write_trace(os.path.join(tmp_path, "run_kernel_trace.csv"), launches)
+    bench.summarize_trace(str(tmp_path), "deferred", "tiny", warmup=2, steps=3)
+    out = capsys.readouterr().out
+    rows = {line.split("(")[1].split(")")[0]: line for line in out.splitlines()
+            if line.startswith("| `")}
+    assert set(rows) == {"local+var", "sync1", "srv", "recon+var"}
+    for key, avg in (("local+var", 7000.0), ("sync1", 4000.0), ("srv", 7530.0),
+                     ("recon+var", 5000.0)):
+        cells = [c.strip() for c in rows[key].split("|")]
+        assert cells[2] == "3", key           # calls
+        assert float(cells[3]) == pytest.approx(avg), key
+    assert "k_local<true, 0, true, 0>" not in out  # the first, pre-sync variant is warmup
