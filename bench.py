@@ -387,6 +387,75 @@ def schedule_run(zo, torch, wl, state, g_in, gb_in, packed, scales, srv_packed, 
             "params_per_s": round(wl.n * wl.steps / (ms / 1000.0), 1)}
 
 
+def _oracle_share(wl, c0, c1, fv, barrier, results):
+    """One process of the chunk-parallel oracle run: chunks [c0, c1) of the
+    shard, inputs generated at their global indices, then (after every
+    process is ready) the same two steps as cpu_baseline, timed."""
+    import numpy as np
+    import oracle as orc
+    import synth
+    from synth import configs as C
+    full = orc.Layout.from_segments(wl.seg_off, wl.chunk)
+    lay = orc.Layout.from_lengths(full.clen[c0:c1])
+    n, e0, w0 = lay.n, int(full.cstart[c0]), int(full.cword[c0])
+    ks = C.ksigma(wl.sigma_g)
+    x0 = synth.normal_host(n, e0, synth.key(0, C.STREAM_X, 0), C.ksigma(wl.sigma_x))
+    g = synth.normal_host(n, e0, synth.key(0, C.STREAM_G, 0), ks, wl.outlier_per_mille,
+                          wl.outlier_factor)
+    gb = synth.normal_host(n, e0, synth.key(0, C.STREAM_GBAR, 0), ks, wl.outlier_per_mille,
+                           wl.outlier_factor)
+    W = wl.world
+    base = np.float32(0.8 * wl.sigma_g if fv else 2 * 1e-4 * 0.18 * wl.sigma_g)
+    pw = np.stack([synth.bits_host(lay.nwords, w0, synth.key(w, C.STREAM_BITS, 1))
+                   for w in range(1, W)])
+    ps = np.stack([synth.scales_host(c1 - c0, c0, synth.key(w, C.STREAM_SCALES, 1), base)
+                   for w in range(1, W)])
+    gam = np.float32(1e-4)
+    if fv:
+        worker = orc.FVWorker(lay, x0, wl.beta1, wl.beta2, wl.eps)
+        barrier.wait()
+        t0 = time.perf_counter()
+        worker.step(gam, g, True, gbar=gb)
+        worker.step(gam, g, False, peer_words=pw, peer_scales=ps)
+    else:
+        worker = orc.Worker(lay, x0, wl.beta1, wl.beta2, wl.eps)
+        barrier.wait()
+        t0 = time.perf_counter()
+        worker.step(gam, g, False, True, gbar=gb)
+        worker.step(gam, g, True, True, gbar=gb, peer_words=pw, peer_scales=ps)
+    results.put((n, time.perf_counter() - t0))
+
+
+def cpu_baseline_parallel(wl, sample_chunks, fv, cores):
+    """The oracle as it stands, chunk-parallel on `cores` host cores: the
+    sample's chunks split into contiguous ranges, one forked process each
+    (every computation is chunk-local, so the ranges' results are the full
+    run's).  Must run before this process initialises the GPU: the children
+    are forks that never exec and never touch the GPU."""
+    import multiprocessing as mp
+    from oracle import Layout
+    ctx = mp.get_context("fork")
+    full = Layout.from_segments(wl.seg_off, wl.chunk)
+    nch = min(sample_chunks, full.nchunks)
+    cores = max(1, min(cores, nch))
+    cuts = [nch * k // cores for k in range(cores + 1)]
+    barrier, results = ctx.Barrier(cores), ctx.Queue()
+    procs = [ctx.Process(target=_oracle_share,
+                         args=(wl, cuts[k], cuts[k + 1], fv, barrier, results))
+             for k in range(cores)]
+    for p in procs:
+        p.start()
+    got = [results.get() for _ in procs]
+    for p in procs:
+        p.join()
+    n = sum(r[0] for r in got)
+    dt = max(r[1] for r in got)
+    return {"value": 2 * n / dt, "unit": "params/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {nch} chunks ({n} params), split into {cores} contiguous chunk "
+                      f"ranges, one process each: the same two steps; slowest process "
+                      f"{dt:.2f} s"}
+
+
 def cpu_baseline(wl, sample_chunks, fv=False):
     """Time the oracle on the first `sample_chunks` chunks of the shard: one
     local step with variance update and one sync step with variance update
@@ -453,6 +522,9 @@ def main():
     ap.add_argument("--cpu-sample-chunks", type=int, default=2048,
                     help="chunks of the shard the CPU oracle is timed on (GPT-2: 33.5M params)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-cores", type=int,
+                    default=min(16, len(os.sched_getaffinity(0))),
+                    help="processes of the chunk-parallel oracle run (1: skip it)")
     ap.add_argument("--eager-sync-writes", action="store_true",
                     help="the reconstruction writes x and u at every sync")
     ap.add_argument("--grad-dtype", choices=("f32", "f16", "bf16"), default="f32",
@@ -489,10 +561,19 @@ def main():
               f"part of this build (asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
 
+    from synth import configs as C
+    wl = C.get(args.workload)
+    # the chunk-parallel oracle run forks, so it runs before anything here
+    # initialises the GPU
+    cpu_parallel = None
+    if not args.no_cpu_baseline and args.cpu_cores > 1:
+        print(f"[bench] timing the CPU oracle on {args.cpu_cores} cores", file=sys.stderr,
+              flush=True)
+        cpu_parallel = cpu_baseline_parallel(wl, args.cpu_sample_chunks, fv, args.cpu_cores)
+
     import torch
     import paper_2202_06009_amd as zo
     import synth
-    from synth import configs as C
 
     zo.lib()
     if args.copy_calibration:
@@ -504,7 +585,6 @@ def main():
         torch.cuda.synchronize()
         del src, dst
         torch.cuda.empty_cache()
-    wl = C.get(args.workload)
     d, W = wl.n, wl.world
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
@@ -683,6 +763,7 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_chunks, fv)
+        out["cpu_baseline_all_cores"] = cpu_parallel
     print(json.dumps(out), flush=True)
 
 
