@@ -426,6 +426,21 @@ def _oracle_share(wl, c0, c1, fv, barrier, results):
     results.put((n, time.perf_counter() - t0))
 
 
+def gpu_device_open():
+    """Whether this process already holds the GPU device open (a profiler
+    preloaded into it may initialise the GPU before the program starts)."""
+    try:
+        for fd in os.listdir("/proc/self/fd"):
+            try:
+                if os.readlink(f"/proc/self/fd/{fd}") == "/dev/kfd":
+                    return True
+            except OSError:
+                pass
+    except OSError:
+        return True  # cannot tell: assume it is
+    return False
+
+
 def cpu_baseline_parallel(wl, sample_chunks, fv, cores):
     """The oracle as it stands, chunk-parallel on `cores` host cores: the
     sample's chunks split into contiguous ranges, one forked process each
@@ -566,7 +581,7 @@ def main():
     # the chunk-parallel oracle run forks, so it runs before anything here
     # initialises the GPU
     cpu_parallel = None
-    if not args.no_cpu_baseline and args.cpu_cores > 1:
+    if not args.no_cpu_baseline and args.cpu_cores > 1 and not gpu_device_open():
         print(f"[bench] timing the CPU oracle on {args.cpu_cores} cores", file=sys.stderr,
               flush=True)
         cpu_parallel = cpu_baseline_parallel(wl, args.cpu_sample_chunks, fv, args.cpu_cores)
