@@ -1,4 +1,5 @@
-"""GPU edge cases: call order, argument errors, an empty shard, a shard of
+"""GPU edge cases: call order, argument errors, an empty shard, zero-gradient
+segments, a shard of
 more than 2^31 parameters, the server restricted to a chunk range, pad bits on
 input, the exact-sum condition, run-to-run determinism."""
 import numpy as np
@@ -113,6 +114,59 @@ def test_shard_beyond_2_31_elements(torch_cuda):
     for t, bad in enumerate(report):
         assert not bad, f"mismatch after step {t - 1}: {bad}"
     assert inexact == 0
+
+
+@pytest.mark.parametrize("defer", [False, True], ids=["eager", "defer"])
+def test_zero_gradient_segments(torch_cuda, defer):
+    """Parameters whose gradient is exactly zero for the whole run (untouched
+    embedding rows, frozen tensors): a segment of +0 and one of -0 gradients
+    (and averaged gradients) next to a normal one, W = 3.  Up to the first
+    sync their momentum and buffer stay zero, so that sync compresses exact
+    zeros (scale 0, every sign +1: sign(+0) = sign(-0) = +1) and the server
+    average there is the peers' alone; afterwards their momentum is the
+    reconstructed average.  Every state and output against the oracle fed the
+    same zeros, after every step."""
+    import harness
+    zero, negzero = (0, 4096), (7096, 8096)
+    wl = _wl(segs=(4096, 3000, 1000), chunk=1024, world=3, T=8, tu=(1, 3, 4, 7),
+             tv=(0, 1, 2, 5))
+    grun = harness.GpuRun(wl, defer=defer)
+    orun = harness.OracleRun(wl)
+    fill = grun.fill_inputs
+
+    def fill_zero(t):
+        fill(t)
+        for buf in (grun.g, grun.gb):  # binary32: these are the tensors handed over
+            buf[zero[0]:zero[1]] = 0.0
+            buf[negzero[0]:negzero[1]] = -0.0
+
+    def zeroed(f):
+        def h(t):
+            a = np.array(f(t), dtype=np.float32, copy=True)
+            a[zero[0]:zero[1]] = 0.0
+            a[negzero[0]:negzero[1]] = -0.0
+            return a
+        return h
+
+    grun.fill_inputs = fill_zero
+    orun.grad, orun.gbar = zeroed(orun.grad), zeroed(orun.gbar)
+    cmp_ = harness.Comparator(grun, orun)
+    try:
+        assert not cmp_.check(-1, None)
+        for t in range(wl.steps):
+            grun.step(t)
+            out = orun.step(t)
+            bad = cmp_.check(t, out)
+            assert not bad, f"step {t}: {bad}"
+            if t == min(wl.tu):
+                # the +0 segment's four chunks: scale 0, all 64 words all ones
+                own_s = grun.scales[0][:4].cpu().numpy()
+                assert (own_s == 0).all(), own_s
+                assert (grun.packed[0][:4 * 16].cpu().numpy() == -1).all()
+                assert not orun.worker.err[zero[0]:zero[1]].any()
+        assert grun.opt.inexact_chunks() == 0
+    finally:
+        grun.close()
 
 
 def test_server_range_matches_single_server(torch_cuda):
