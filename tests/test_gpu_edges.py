@@ -1,7 +1,7 @@
 """GPU edge cases: call order, argument errors, an empty shard, zero-gradient
-segments, a shard of
-more than 2^31 parameters, the server restricted to a chunk range, pad bits on
-input, the exact-sum condition, run-to-run determinism."""
+segments, a shard of more than 2^31 parameters, the server restricted to a
+chunk range, pad bits on input, the exact-sum condition, run-to-run
+determinism."""
 import numpy as np
 import pytest
 
