@@ -6,6 +6,8 @@ every step of a run.  The contract allows a relative error of 1e-6 on the
 binary32 states; the kernels are built to reproduce the oracle's rounding
 exactly, so these tests demand equality (with -0 == +0), which implies it.
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -251,6 +253,21 @@ def test_workload_sampled(torch_cuda, name):
     _log(f"{name}: {len(ids)} chunks sampled, {int(lay.clen[ids].sum())} elements, "
          f"{int((lay.clen[ids] != wl.chunk).sum())} ragged")
     report, inexact = harness.run_parity(wl, chunk_ids=ids, log=_log)
+    _assert_clean(report, inexact)
+
+
+@pytest.mark.skipif(os.environ.get("ZO_FULL_SHARD") != "1",
+                    reason="a whole-shard oracle run takes minutes; set ZO_FULL_SHARD=1")
+@pytest.mark.timeout(1800)
+@pytest.mark.parametrize("name", ["resnet50", "bert-base"])
+def test_workload_full_shard(torch_cuda, name):
+    """ResNet-50 and BERT-Base with the oracle over the whole shard (every
+    element, word and scale compared after every step of the workload's
+    schedule), not a sample of chunks."""
+    import harness
+    wl = C.get(name)
+    _log(f"{name}: full shard, {wl.n} params, W={wl.world}, {wl.steps} steps")
+    report, inexact = harness.run_parity(wl, log=_log)
     _assert_clean(report, inexact)
 
 
