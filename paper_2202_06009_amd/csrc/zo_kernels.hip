@@ -591,6 +591,25 @@ __device__ __forceinline__ uint32_t byte_x8(uint32_t x)
     return r;
 }
 
+// Workgroups are dealt to the GPU's 8 XCDs round-robin (workgroup i to XCD
+// i % 8), and each XCD has its own L2.  With the grid padded to a multiple
+// of 8 workgroups, block i takes block number (i % 8) * (grid / 8) + i / 8:
+// every XCD walks a contiguous run of blocks in order, so neighbouring
+// chunks share its L2 (in every worker's row the cache line that straddles
+// two chunks' words, and each line holding 32 chunks' scales).
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ int64_t xcd_block()
+{
+    const int64_t per = gridDim.x / kXcds;
+    return (int64_t)(blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+}
+
+static inline unsigned xcd_grid(unsigned blocks)
+{
+    return (blocks + kXcds - 1) / kXcds * kXcds;
+}
+
 // Load the 8 dwords of worker group g (workers beyond W read as 0).  Plain
 // loads: the nontemporal hint measured no faster for these dword accesses.
 // a value the whole wave agrees on, moved to scalar registers: a load at
@@ -692,7 +711,7 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
 
     const int q = CPW == 1 ? 0 : (int)threadIdx.x / LD;
     const int lc = CPW == 1 ? (int)threadIdx.x : (int)threadIdx.x % LD;
-    const int64_t cbase = (int64_t)blockIdx.x * CPW;
+    const int64_t cbase = xcd_block() * CPW;
     const int64_t cr = cbase + q;
     const bool active = cr < nch;
     const int64_t c = c0 + (active ? cr : 0);
@@ -739,21 +758,27 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
     __syncthreads();
     {
         // CPW * G * 256 entries over LD * CPW threads, kPer each (both powers
-        // of two; a thread with no entry of its own repeats one): every read
-        // is issued before the first add
+        // of two; a thread with no entry of its own repeats one), in batches
+        // of at most 8 whose reads are all issued before the first add (a
+        // narrow workgroup has thousands of entries per thread: one batch at
+        // a time keeps them out of scratch memory)
         constexpr int kTotal = CPW * G * 256, kThreads = LD * CPW;
         constexpr int kPer = kTotal >= kThreads ? kTotal / kThreads : 1;
-        double lo[kPer], hi[kPer];
+        constexpr int kBatch = kPer < 8 ? kPer : 8;
+#pragma unroll 1
+        for (int k0 = 0; k0 < kPer; k0 += kBatch) {
+            double lo[kBatch], hi[kBatch];
 #pragma unroll
-        for (int k = 0; k < kPer; ++k) {
-            const int i = ((int)threadIdx.x + k * kThreads) % kTotal;
-            const int qg = i >> 8, b = i & 255;  // qg = chunk * G + group
-            lo[k] = half[32 * qg + (b & 15)];
-            hi[k] = half[32 * qg + 16 + (b >> 4)];
+            for (int k = 0; k < kBatch; ++k) {
+                const int i = ((int)threadIdx.x + (k0 + k) * kThreads) % kTotal;
+                const int qg = i >> 8, b = i & 255;  // qg = chunk * G + group
+                lo[k] = half[32 * qg + (b & 15)];
+                hi[k] = half[32 * qg + 16 + (b >> 4)];
+            }
+#pragma unroll
+            for (int k = 0; k < kBatch; ++k)
+                tab[((int)threadIdx.x + (k0 + k) * kThreads) % kTotal] = lo[k] + hi[k];
         }
-#pragma unroll
-        for (int k = 0; k < kPer; ++k)
-            tab[((int)threadIdx.x + k * kThreads) % kTotal] = lo[k] + hi[k];
     }
     __syncthreads();
     const char *mytab = reinterpret_cast<const char *>(tab) + (size_t)q * G * 2048;
@@ -1239,7 +1264,7 @@ static hipError_t go_srv_lut(const uint64_t *packed, const float *scales, int W,
                              int pow2, hipStream_t st)
 {
     constexpr int CPW = srv_chunks_per_block(LD, G);
-    hipLaunchKernelGGL((k_srv_lut<LD, G>), dim3(grid_for(nch, CPW)), dim3(LD * CPW), 0, st,
+    hipLaunchKernelGGL((k_srv_lut<LD, G>), dim3(xcd_grid(grid_for(nch, CPW))), dim3(LD * CPW), 0, st,
                        reinterpret_cast<const uint32_t *>(packed), scales, W, wstride, cstride,
                        ch, c0, nch, word0, elem0, srv_err, reinterpret_cast<uint32_t *>(srv_packed),
                        srv_scales, avg, flags, inv_w, pow2);
