@@ -282,12 +282,28 @@ def zo_diag_stream(srcs, dsts, stream=None):
         raise ZoError(rc, "zo_diag_stream")
 
 
+_TORCH_GRAD = {"f32": "float32", "f16": "float16", "bf16": "bfloat16"}
+
+
+def _need(t, what, dtype, n):
+    """A tensor of torch dtype `dtype` with at least n elements (the C ABI
+    takes bare pointers, so a short buffer would be read or written past
+    its end on the device)."""
+    if t is None:
+        raise ValueError(f"{what}: a tensor is required")
+    if str(t.dtype).replace("torch.", "") != dtype:
+        raise ValueError(f"{what}: expected {dtype}, got {t.dtype}")
+    if t.numel() < n:
+        raise ValueError(f"{what}: needs at least {n} elements, has {t.numel()}")
+
+
 class ZoAdam:
     """One worker's 0/1 Adam optimizer state on one GPU (a handle of the C ABI).
 
     ``state`` maps x, m, v, u, err, srv_err, anchor to float32 device tensors;
     x holds x_0.  The handle enqueues on ``stream`` (torch's current stream by
-    default)."""
+    default).  Every method checks its tensors' element types and sizes
+    against the configuration before anything reaches the device."""
 
     def __init__(self, *, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), state,
                  srv_chunk_begin=0, srv_chunk_end=-1, defer_sync_writes=False,
@@ -297,8 +313,44 @@ class ZoAdam:
                         srv_chunk_begin=srv_chunk_begin, srv_chunk_end=srv_chunk_end,
                         defer_sync_writes=defer_sync_writes, algorithm=algorithm,
                         grad_dtype=grad_dtype)
+        self.h = None
+        self._sizes()
+        n = self.n
+        fv = algorithm == "frozen-variance"
+        for k in ("x", "m", "v", "err", "u", "anchor"):
+            if fv and k in ("u", "anchor") and state.get(k) is None:
+                continue
+            if n:
+                _need(state.get(k), f"state[{k!r}]", "float32", n)
+        if self.r_elems:
+            _need(state.get("srv_err"), "state['srv_err']", "float32", self.r_elems)
         self.state = state
         self.h = zo_adam_init(self.cfg, state, stream)
+
+    def _sizes(self):
+        """Shard length, chunks, packed words and the server range, from the
+        host planning helpers (an invalid configuration is left to
+        zo_adam_init to reject)."""
+        c = self.cfg
+        start, ln, word, nwords = zo_plan_chunks(c["seg_off"], c["chunk"])
+        nch = len(ln)
+        self.n, self.nchunks, self.nwords = int(c["seg_off"][-1]), nch, int(nwords)
+        c0 = int(c["srv_chunk_begin"])
+        c1 = nch if c["srv_chunk_end"] < 0 else int(c["srv_chunk_end"])
+        self.r_chunks = self.r_words = self.r_elems = 0
+        if 0 <= c0 < c1 <= nch:
+            self.r_chunks = c1 - c0
+            self.r_words = word[c1 - 1] + (ln[c1 - 1] + 63) // 64 - word[c0]
+            self.r_elems = start[c1 - 1] + ln[c1 - 1] - start[c0]
+
+    def _grad(self, t, what):
+        if self.n:
+            _need(t, what, _TORCH_GRAD[self.cfg["grad_dtype"]], self.n)
+
+    def _server_out(self, srv_packed, srv_scales):
+        if self.nchunks:
+            _need(srv_packed, "srv_packed", "int64", self.nwords)
+            _need(srv_scales, "srv_scales", "float32", self.nchunks)
 
     def close(self):
         if self.h is not None:
@@ -318,21 +370,41 @@ class ZoAdam:
 
     # the six hot-path calls
     def local_step(self, t, gamma, g, gbar=None):
+        self._grad(g, "g")
+        if gbar is not None:
+            self._grad(gbar, "gbar")
         zo_local_step(self.h, t, gamma, g, gbar)
 
     def compress_pack_ef(self, t, gamma, g, packed0, scales0):
+        if g is not None:
+            self._grad(g, "g")
+        if self.nchunks:
+            _need(packed0, "packed0", "int64", self.nwords)
+            _need(scales0, "scales0", "float32", self.nchunks)
         zo_compress_pack_ef(self.h, t, gamma, g, packed0, scales0)
 
     def unpack_average(self, t, packed, scales, srv_packed, srv_scales, avg_debug=None):
+        W = int(self.cfg["world"])
+        if self.r_chunks:
+            _need(packed, "packed", "int64", W * self.r_words)
+            _need(scales, "scales", "float32", W * self.r_chunks)
+        self._server_out(srv_packed, srv_scales)
+        if avg_debug is not None:
+            _need(avg_debug, "avg_debug", "float32", self.r_elems)
         zo_unpack_average(self.h, t, packed, scales, srv_packed, srv_scales, avg_debug)
 
     def sync_update(self, t, srv_packed, srv_scales, gbar=None):
+        self._server_out(srv_packed, srv_scales)
+        if gbar is not None:
+            self._grad(gbar, "gbar")
         zo_sync_update(self.h, t, srv_packed, srv_scales, gbar)
 
     def variance_update(self, t, gbar):
+        self._grad(gbar, "gbar")
         zo_variance_update(self.h, t, gbar)
 
     def fullprec_step(self, t, gamma, gbar):
+        self._grad(gbar, "gbar")
         zo_fullprec_step(self.h, t, gamma, gbar)
 
     def materialize(self):

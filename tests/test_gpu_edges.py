@@ -42,9 +42,24 @@ def test_call_order_is_enforced(torch_cuda):
         with pytest.raises(zo.ZoError) as e:       # gamma must be > 0
             o.local_step(0, 0.0, g)
         assert e.value.status == zo.ZO_EINVAL
-        with pytest.raises(zo.ZoError) as e:       # misaligned gradient
-            o.local_step(0, 1e-4, g[1:])
+        # a full-length gradient at an address that is not 16-byte aligned
+        g_off = torch_cuda.empty(g.numel() + 1, dtype=g.dtype, device=g.device)[1:]
+        g_off.copy_(g)
+        with pytest.raises(zo.ZoError) as e:
+            o.local_step(0, 1e-4, g_off)
         assert e.value.status == zo.ZO_EALIGN
+        # the binding checks element types and sizes before the C ABI (which
+        # takes bare pointers) is called
+        for bad in (g[:-4], g.double(), g.half()):
+            with pytest.raises(ValueError):
+                o.local_step(0, 1e-4, bad)
+        with pytest.raises(ValueError):
+            o.compress_pack_ef(0, 1e-4, g, run.packed[0][:-1], run.scales[0])
+        with pytest.raises(ValueError):
+            o.unpack_average(0, run.packed[:-1], run.scales, run.srv_packed, run.srv_scales)
+        with pytest.raises(ValueError):
+            o.sync_update(0, run.srv_packed, run.srv_scales.double(), None)
+        assert o.next_step == 0
         o.local_step(0, 1e-4, g)                   # t = 0 in T_v: variance still due
         with pytest.raises(zo.ZoError) as e:
             o.local_step(1, 1e-4, g)
