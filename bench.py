@@ -155,7 +155,7 @@ def summarize_trace(trace_dir, mode, workload, warmup, steps):
               f"{model[key] / 1e9:.3f} | {gbs:.0f} | {100 * gbs / HBM_PEAK_GBS:.1f} |")
 
 
-def summarize_pmc(fetch_dir, write_dir, out_path, mode):
+def summarize_pmc(fetch_dir, write_dir, out_path, mode, workload):
     """Turn two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over
     `bench.py --copy-calibration` into per-launch HBM traffic, each counter
     scaled by what it reads for the calibration copy of COPY_BYTES.
@@ -187,7 +187,8 @@ def summarize_pmc(fetch_dir, write_dir, out_path, mode):
         f, w = factors[kind]["fetch"], factors[kind]["write"]
         kernels[key] = {"fetch_kib": fetch[key], "write_kib": write[key], "access": kind,
                         "traffic_bytes": 1024.0 * (fetch[key] * f + write[key] * w)}
-    out = {"source_sha256": source_hash(), "mode": mode, "copy_bytes": COPY_BYTES,
+    out = {"source_sha256": source_hash(), "mode": mode, "workload": workload,
+           "copy_bytes": COPY_BYTES,
            "copy_kib": {k: {"fetch": fetch[f"copy_{k}"], "write": write[f"copy_{k}"]}
                         for k in ("nt", "plain")},
            "factors": factors, "kernels": kernels}
@@ -196,15 +197,17 @@ def summarize_pmc(fetch_dir, write_dir, out_path, mode):
     print(json.dumps(out, indent=1))
 
 
-def measured_traffic(kernel, mode):
+def measured_traffic(kernel, mode, workload):
     """HBM bytes per launch from the committed counter summary, or None when
-    it is missing or was taken on different kernel source or another mode."""
+    it is missing or was taken on different kernel source, in another mode or
+    on another workload."""
     try:
         with open(TRAFFIC_FILE) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
-    if t.get("source_sha256") != source_hash() or t.get("mode") != mode:
+    if (t.get("source_sha256") != source_hash() or t.get("mode") != mode
+            or t.get("workload") != workload):
         return None
     if kernel not in t.get("kernels", {}):
         return None
@@ -563,7 +566,8 @@ def main():
     if args.grad_dtype != "f32":
         mode += f"/{args.grad_dtype}"
     if args.summarize_pmc:
-        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], TRAFFIC_FILE, mode)
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], TRAFFIC_FILE, mode,
+                      args.workload)
         return
     if args.summarize_counters:
         summarize_counters(args.summarize_counters, mode)
@@ -729,7 +733,7 @@ def main():
                for n in names}
     dom = max(names, key=lambda n: per_kernel[n])
     step_bytes = sum(bytes_.values())
-    tb = measured_traffic(dom, mode)
+    tb = measured_traffic(dom, mode, wl.name)
     traffic_gb = None if tb is None else round(tb / 1e9, 3)
     out = {
         "metric": "0/1 Adam step params/sec and achieved HBM GB/s (% of peak), 1 MI355X",

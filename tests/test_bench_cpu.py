@@ -81,3 +81,22 @@ def test_trace_summary_keeps_the_timed_dispatches(tmp_path, capsys):
         assert cells[2] == "3", key           # calls
         assert float(cells[3]) == pytest.approx(avg), key
     assert "k_local<true, 0, true, 0>" not in out  # the first, pre-sync variant is warmup
+
+
+def test_traffic_summary_only_for_its_workload_and_source(tmp_path, monkeypatch):
+    """The measured traffic is reported only for the workload, mode and kernel
+    source the counters were taken on."""
+    import json
+    f = tmp_path / "traffic.json"
+    f.write_text(json.dumps({"source_sha256": bench.source_hash(), "mode": "deferred",
+                             "workload": "gpt2-1.5b",
+                             "kernels": {"local+var": {"traffic_bytes": 1.0}}}))
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
+    assert bench.measured_traffic("local+var", "deferred", "gpt2-1.5b") == 1.0
+    assert bench.measured_traffic("local+var", "deferred", "bert-base") is None
+    assert bench.measured_traffic("local+var", "eager", "gpt2-1.5b") is None
+    assert bench.measured_traffic("srv", "deferred", "gpt2-1.5b") is None
+    f.write_text(json.dumps({"source_sha256": "0" * 64, "mode": "deferred",
+                             "workload": "gpt2-1.5b",
+                             "kernels": {"local+var": {"traffic_bytes": 1.0}}}))
+    assert bench.measured_traffic("local+var", "deferred", "gpt2-1.5b") is None
