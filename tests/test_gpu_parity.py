@@ -115,6 +115,8 @@ SMALL = [
     ([40000, 8192, 8188], 8192, 4),          # V = 8
     ([70000, 16384, 16380, 4], 16384, 3),    # V = 16
     ([5000, 1000, 96], 1024, 9),             # two worker groups, the second partial
+    ([3000, 1024, 1020, 8], 1024, 40),       # G = 8 tables, groups 5..7 past the last worker
+    ([20000, 16384, 4], 16384, 100),         # G = 16 at the GPT-2 chunk, 13 groups used
     ([5000, 1000], 1024, 300),               # tables beyond the LDS budget: plain server
 ]
 
