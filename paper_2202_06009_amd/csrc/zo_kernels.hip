@@ -652,7 +652,9 @@ constexpr int srv_chunks_per_block(int LD, int G)
 {
     const int fill = LD >= 64 ? 1 : 64 / LD;
     const int fit = 32 / G > 1 ? 32 / G : 1;
-    return fill < fit ? fill : fit;
+    int c = fill < fit ? fill : fit;
+    while (c & (c - 1)) c &= c - 1;  // a power of two (G need not be one)
+    return c;
 }
 
 // Eight table lookups (byte C of the eight transposed registers) added to
@@ -757,13 +759,14 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
     }
     __syncthreads();
     {
-        // CPW * G * 256 entries over LD * CPW threads, kPer each (both powers
-        // of two; a thread with no entry of its own repeats one), in batches
+        // CPW * G * 256 entries over LD * CPW threads, kPer = the ceiling of
+        // their ratio each (a thread past the last entry repeats one from the
+        // start: the same value written twice), in batches
         // of at most 8 whose reads are all issued before the first add (a
         // narrow workgroup has thousands of entries per thread: one batch at
         // a time keeps them out of scratch memory)
         constexpr int kTotal = CPW * G * 256, kThreads = LD * CPW;
-        constexpr int kPer = kTotal >= kThreads ? kTotal / kThreads : 1;
+        constexpr int kPer = (kTotal + kThreads - 1) / kThreads;
         constexpr int kBatch = kPer < 8 ? kPer : 8;
 #pragma unroll 1
         for (int k0 = 0; k0 < kPer; k0 += kBatch) {
@@ -1282,10 +1285,18 @@ static hipError_t srv_lut_ld(int LD, const uint64_t *packed, const float *scales
     case L:                                                                                    \
         return go_srv_lut<L, G>(packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, \
                                 srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
-    switch (LD) {
-        ZO_SRV_LD(1) ZO_SRV_LD(2) ZO_SRV_LD(4) ZO_SRV_LD(8) ZO_SRV_LD(16) ZO_SRV_LD(32)
-        ZO_SRV_LD(64) ZO_SRV_LD(128) ZO_SRV_LD(256) ZO_SRV_LD(512)
-    default: return hipErrorInvalidValue;
+    if constexpr ((G & (G - 1)) != 0) {
+        // groups counted exactly only for chunks of at least 64 dwords
+        switch (LD) {
+            ZO_SRV_LD(64) ZO_SRV_LD(128) ZO_SRV_LD(256) ZO_SRV_LD(512)
+        default: return hipErrorInvalidValue;
+        }
+    } else {
+        switch (LD) {
+            ZO_SRV_LD(1) ZO_SRV_LD(2) ZO_SRV_LD(4) ZO_SRV_LD(8) ZO_SRV_LD(16) ZO_SRV_LD(32)
+            ZO_SRV_LD(64) ZO_SRV_LD(128) ZO_SRV_LD(256) ZO_SRV_LD(512)
+        default: return hipErrorInvalidValue;
+        }
     }
 #undef ZO_SRV_LD
 }
@@ -1298,7 +1309,10 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
 {
     if (nch == 0) return hipSuccess;
     const Geometry sg = srv_geometry_for(chunk);
-    const int G = next_pow2((W + 7) / 8);
+    // worker groups of 8 (the last one may be partial); chunks of fewer than
+    // 64 dwords round the count up to a power of two (fewer instantiations,
+    // the extra groups' tables are zero)
+    const int G = sg.L >= 64 ? (W + 7) / 8 : next_pow2((W + 7) / 8);
     const int cpw = srv_chunks_per_block(sg.L, G);
     const size_t tab = (size_t)cpw * G * 2048, xpose = (size_t)cpw * sg.L * 128;
     const size_t lds = (tab > xpose ? tab : xpose) + (size_t)cpw * G * 32 + (size_t)cpw * G * 256 + 256;
@@ -1320,8 +1334,19 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
     switch (G) {
     case 1: return srv_lut_ld<1>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
     case 2: return srv_lut_ld<2>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 3: return srv_lut_ld<3>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
     case 4: return srv_lut_ld<4>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 5: return srv_lut_ld<5>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 6: return srv_lut_ld<6>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 7: return srv_lut_ld<7>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
     case 8: return srv_lut_ld<8>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 9: return srv_lut_ld<9>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 10: return srv_lut_ld<10>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 11: return srv_lut_ld<11>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 12: return srv_lut_ld<12>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 13: return srv_lut_ld<13>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 14: return srv_lut_ld<14>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
+    case 15: return srv_lut_ld<15>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
     case 16: return srv_lut_ld<16>(sg.L, packed, scales, W, wstride, cstride, ch, c0, nch, word0, elem0, srv_err, srv_packed, srv_scales, avg, flags, inv_w, pow2, st);
     default: return hipErrorInvalidValue;
     }
