@@ -116,7 +116,9 @@ SMALL = [
     ([70000, 16384, 16380, 4], 16384, 3),    # V = 16
     ([5000, 1000, 96], 1024, 9),             # two worker groups, the second partial
     ([3000, 1024, 1020, 8], 1024, 40),       # G = 8 tables, groups 5..7 past the last worker
-    ([20000, 16384, 4], 16384, 100),         # G = 16 at the GPT-2 chunk, 13 groups used
+    ([20000, 16384, 4], 16384, 100),         # G = 13 at the GPT-2 chunk, the last of 4 workers
+    ([6000, 2048, 2044], 2048, 20),          # G = 3 at 64 lanes, the last of 4 workers
+    ([8192, 4096, 100], 4096, 72),           # G = 9 at 128 lanes
     ([5000, 1000], 1024, 300),               # tables beyond the LDS budget: plain server
 ]
 
