@@ -91,7 +91,7 @@ def test_chunk_plan_matches_oracle_layout(name):
     assert nw == lay.nwords
 
 
-def test_chunk_plan_counts_match_survey_shapes():
+def test_chunk_plan_counts_match_workload_shapes():
     expect = {"tiny": (512, 0), "bert-base": (26823, 125), "bert-large": (41116, 245),
               "resnet50": (25021, 86), "gpt2-1.5b": (95442, 483)}
     for name, (nch, partial) in expect.items():
