@@ -169,7 +169,11 @@ int zo_adam_init(zo_adam **h, const zo_config *cfg, const zo_state *st, hipStrea
 /* Release the handle and its device memory.  Waits for the stream. */
 int zo_adam_destroy(zo_adam *h);
 
-/* Change the stream later calls enqueue on. */
+/* Change the stream later calls enqueue on.  Work already enqueued on the
+ * previous stream is not waited for: the caller orders the two streams (an
+ * event recorded on the old one and waited on by the new one) before the next
+ * call, since every call reads what the previous one wrote.  zo_adam_destroy
+ * waits only for the current stream. */
 int zo_set_stream(zo_adam *h, hipStream_t stream);
 
 /*
