@@ -646,12 +646,19 @@ __device__ __forceinline__ void load_group(uint32_t (&x)[8], const uint32_t *pac
 // registers for only a few groups).
 constexpr int kSrvPrefetch = 2;
 
+// Chunks of fewer than 64 dwords (several chunks per wave) look up the two
+// 16-entry half tables of each group directly instead of building the
+// 256-entry table from them: the build would cost as much as the lookups, and
+// the smaller tables leave LDS for more waves per CU.
+constexpr bool srv_nibble(int LD) { return LD < 64; }
+
 // Chunks per workgroup of the LUT server: enough chunks to fill a wave when a
 // chunk has fewer than 64 dwords, as long as their tables fit in 64 KB.
 constexpr int srv_chunks_per_block(int LD, int G)
 {
     const int fill = LD >= 64 ? 1 : 64 / LD;
-    const int fit = 32 / G > 1 ? 32 / G : 1;
+    const int per = srv_nibble(LD) ? 256 : 32;  // chunks of G groups' tables in 64 KB, times G
+    const int fit = per / G > 1 ? per / G : 1;
     int c = fill < fit ? fill : fit;
     while (c & (c - 1)) c &= c - 1;  // a power of two (G need not be one)
     return c;
@@ -676,6 +683,30 @@ __device__ __forceinline__ void lookup8(double (&acc)[32], const uint32_t (&x)[8
                  : "memory");
 }
 
+// The same for the half tables at hg (16 entries for the low nibble of a
+// worker byte, workers 8g..8g+3, then 16 for the high nibble): two lookups per
+// element; every partial sum is exact, so the order of the adds does not
+// matter.
+template <int C>
+__device__ __forceinline__ void lookup8_nib(double (&acc)[32], const uint32_t (&x)[8],
+                                            const char *hg)
+{
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        // nibble times 8 (a byte offset into its 128-byte table)
+        const uint32_t lo = C == 0 ? (x[k] << 3) & 0x78u : (x[k] >> (8 * C - 3)) & 0x78u;
+        const uint32_t hi = (x[k] >> (8 * C + 1)) & 0x78u;
+        acc[8 * C + k] += *reinterpret_cast<const double *>(hg + lo);
+        acc[8 * C + k] += *reinterpret_cast<const double *>(hg + 128 + hi);
+    }
+    asm volatile(""
+                 : "+v"(acc[8 * C + 0]), "+v"(acc[8 * C + 1]), "+v"(acc[8 * C + 2]),
+                   "+v"(acc[8 * C + 3]), "+v"(acc[8 * C + 4]), "+v"(acc[8 * C + 5]),
+                   "+v"(acc[8 * C + 6]), "+v"(acc[8 * C + 7])
+                 :
+                 : "memory");
+}
+
 // Float4 slot of the transpose buffer that holds float4 t of a chunk (t = e/4).
 // Lane j writes the slots 8j..8j+7 of its dword; lanes then read slots in
 // coalesced order.  XOR-ing the slot's low three bits with bits 1..3 of j makes
@@ -689,10 +720,14 @@ __device__ __forceinline__ int xpose_slot(int t)
 // LD lanes per chunk (one packed dword each), G groups of 8 workers (a
 // compile-time count; groups past the last worker hold zero tables), CPW
 // chunks per workgroup.  The tables of chunk q of the workgroup start at byte
-// q*G*2048 of `tab`; with one chunk per workgroup the offset of every lookup is
-// an immediate.
+// q*G*2048 of `tab` (with half tables, q*G*256 of `half`); with one chunk per
+// workgroup the offset of every lookup is an immediate.  With half tables the
+// LDS leaves room for four one-wave workgroups per SIMD: the register budget
+// is held to that (at 1024-element chunks and W = 32, a 20-byte spill; 74
+// instead of 81 us on the ResNet-50 shape).
 template <int LD, int G>
-__global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
+__global__ __launch_bounds__(LD > 64 ? LD : 64)
+__attribute__((amdgpu_waves_per_eu(srv_nibble(LD) ? 4 : 1))) void k_srv_lut(
     const uint32_t *__restrict__ packed32, const float *__restrict__ scales, int W,
     int64_t wstride, int64_t cstride, Chunks ch, int64_t c0, int64_t nch, int64_t word0,
     int64_t elem0, float *__restrict__ srv_err, uint32_t *__restrict__ srv_packed32,
@@ -700,10 +735,11 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
     double inv_w, int w_pow2)
 {
     constexpr int CPW = srv_chunks_per_block(LD, G);
+    constexpr bool kNib = srv_nibble(LD);
     // static arrays: their LDS addresses are link-time constants, so the group
     // offset of every lookup is an instruction immediate.  The tables are dead
     // once the sums are formed; the same memory then transposes the averages.
-    constexpr int kTabBytes = CPW * G * 256 * 8;
+    constexpr int kTabBytes = kNib ? 0 : CPW * G * 256 * 8;
     constexpr int kXposeBytes = CPW * LD * 32 * 4;
     __shared__ double uni[(kTabBytes > kXposeBytes ? kTabBytes : kXposeBytes) / 8];
     __shared__ float sc[CPW * G * 8];  // W <= 8G
@@ -758,7 +794,7 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
         half[i] = t;
     }
     __syncthreads();
-    {
+    if constexpr (!kNib) {
         // CPW * G * 256 entries over LD * CPW threads, kPer = the ceiling of
         // their ratio each (a thread past the last entry repeats one from the
         // start: the same value written twice), in batches
@@ -782,9 +818,10 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
             for (int k = 0; k < kBatch; ++k)
                 tab[((int)threadIdx.x + (k0 + k) * kThreads) % kTotal] = lo[k] + hi[k];
         }
+        __syncthreads();
     }
-    __syncthreads();
-    const char *mytab = reinterpret_cast<const char *>(tab) + (size_t)q * G * 2048;
+    const char *mytab = kNib ? reinterpret_cast<const char *>(half) + (size_t)q * G * 256
+                             : reinterpret_cast<const char *>(tab) + (size_t)q * G * 2048;
 
     // the server error of the lane's elements in the compress layout (lane lc
     // holds the float4s lc + LD*k, k < 8, of its chunk); loaded while the last
@@ -810,12 +847,21 @@ __global__ __launch_bounds__(LD > 64 ? LD : 64) void k_srv_lut(
                                  ws, g + kSrvPrefetch, W, lc);
             uint32_t (&cur)[8] = ring[g % (kSrvPrefetch + 1)];
             transpose8x32(cur);
-            const char *tg = mytab + g * 2048;
-            lookup8<0>(acc, cur, tg);
-            lookup8<1>(acc, cur, tg);
-            lookup8<2>(acc, cur, tg);
-            if (g == G - 1) load_serr();
-            lookup8<3>(acc, cur, tg);
+            if constexpr (kNib) {
+                const char *hg = mytab + g * 256;
+                lookup8_nib<0>(acc, cur, hg);
+                lookup8_nib<1>(acc, cur, hg);
+                lookup8_nib<2>(acc, cur, hg);
+                if (g == G - 1) load_serr();
+                lookup8_nib<3>(acc, cur, hg);
+            } else {
+                const char *tg = mytab + g * 2048;
+                lookup8<0>(acc, cur, tg);
+                lookup8<1>(acc, cur, tg);
+                lookup8<2>(acc, cur, tg);
+                if (g == G - 1) load_serr();
+                lookup8<3>(acc, cur, tg);
+            }
         }
     } else {
         load_serr();
@@ -1314,7 +1360,8 @@ hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const floa
     // the extra groups' tables are zero)
     const int G = sg.L >= 64 ? (W + 7) / 8 : next_pow2((W + 7) / 8);
     const int cpw = srv_chunks_per_block(sg.L, G);
-    const size_t tab = (size_t)cpw * G * 2048, xpose = (size_t)cpw * sg.L * 128;
+    const size_t tab = srv_nibble(sg.L) ? 0 : (size_t)cpw * G * 2048;
+    const size_t xpose = (size_t)cpw * sg.L * 128;
     const size_t lds = (tab > xpose ? tab : xpose) + (size_t)cpw * G * 32 + (size_t)cpw * G * 256 + 256;
     const bool pow2 = (W & (W - 1)) == 0;
     const double inv_w = 1.0 / (double)W;
