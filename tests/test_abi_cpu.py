@@ -9,6 +9,7 @@ import subprocess
 
 import numpy as np
 import pytest
+from hypothesis import given, settings, strategies as st
 
 import paper_2202_06009_amd as zo
 from synth import configs
@@ -89,6 +90,32 @@ def test_chunk_plan_matches_oracle_layout(name):
     np.testing.assert_array_equal(ln, lay.clen)
     np.testing.assert_array_equal(word, lay.cword)
     assert nw == lay.nwords
+
+
+@settings(max_examples=200, deadline=None)
+@given(lens=st.lists(st.integers(0, 3000).map(lambda v: 4 * v), min_size=1, max_size=12),
+       chunk=st.integers(1, 4096).map(lambda v: 4 * v))
+def test_chunk_plan_properties(lens, chunk):
+    """Random segment tables (empty segments, ragged tails, any chunk that is a
+    multiple of 4 up to 16384): the library's plan equals the oracle's, its
+    chunks tile every segment in order without crossing a boundary, and each
+    chunk's packed words start where the previous chunk's 64-element words end."""
+    import oracle as orc
+    seg_off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64).tolist()
+    start, ln, word, nw = zo.zo_plan_chunks(seg_off, chunk)
+    lay = orc.Layout.from_segments(seg_off, chunk)
+    np.testing.assert_array_equal(start, lay.cstart)
+    np.testing.assert_array_equal(ln, lay.clen)
+    np.testing.assert_array_equal(word, lay.cword)
+    assert nw == lay.nwords
+    expect = [(a + k, min(chunk, b - a - k)) for a, b in zip(seg_off[:-1], seg_off[1:])
+              for k in range(0, b - a, chunk)]
+    assert list(zip(start, ln)) == expect
+    w = 0
+    for s0, l0, w0 in zip(start, ln, word):
+        assert w0 == w
+        w += (l0 + 63) // 64
+    assert nw == w
 
 
 def test_chunk_plan_counts_match_workload_shapes():
