@@ -119,6 +119,8 @@ SMALL = [
     ([20000, 16384, 4], 16384, 100),         # G = 13 at the GPT-2 chunk, the last of 4 workers
     ([6000, 2048, 2044], 2048, 20),          # G = 3 at 64 lanes, the last of 4 workers
     ([8192, 4096, 100], 4096, 72),           # G = 9 at 128 lanes
+    ([3000, 500, 12], 256, 128),             # half tables: 8 lanes per chunk, 16 groups
+    ([700, 64, 36], 32, 64),                 # half tables: one lane per chunk, 8 groups
     ([5000, 1000], 1024, 300),               # tables beyond the LDS budget: plain server
 ]
 
