@@ -305,6 +305,33 @@ def stream_mix_ceilings(zo, torch, state, g, gb, d, mode):
     return out
 
 
+def server_pattern(zo, torch, wl, state, packed, W, nwords, reps=4):
+    """The server's access pattern without its arithmetic (zo_diag_server_pattern
+    on a handle over the whole shard, best of the last reps-1 launches): the
+    rate the single server's reads of W packed rows and read-modify-write of
+    its error can reach.  None for chunks of at most 1024 elements."""
+    if wl.chunk <= 1024:
+        return None
+    d = wl.n
+    opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=W, chunk=wl.chunk,
+                    seg_off=wl.seg_off, tv=[], tu=[0], state=state)
+    best = None
+    for rep in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        opt.diag_server_pattern(packed)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        if rep and (best is None or ms < best):
+            best = ms
+    opt.close()
+    gb = (W * nwords * 8 + 8.0 * d) / 1e9
+    return {"ms": round(best, 4), "gb_per_launch": round(gb, 3),
+            "gbs": round(gb / (best / 1000.0), 1),
+            "frac": round(gb / (best / 1000.0) / HBM_PEAK_GBS, 4)}
+
+
 def server_share(zo, torch, wl, state, g_in, packed, scales, srv_packed, srv_scales, W, reps=10):
     """The server at its per-GPU shape under the sharded design: GPU k = W/2
     serves a chunk-aligned range of about d/W elements, whose W-slot input
@@ -695,7 +722,7 @@ def main():
     # schedule run launch the same kernels at other sizes, the ceiling the
     # same copy kernel).
     extras = not args.copy_calibration
-    share = sched = mix = None
+    share = sched = mix = pattern = None
     copy_gbs = float("nan")
     if extras and not fv:
         share = server_share(zo, torch, wl, state, g_in, packed, scales, srv_packed, srv_scales,
@@ -716,6 +743,7 @@ def main():
         # (the diagnostic streams binary32 arrays: no like-for-like mix for 16-bit gradients)
         if args.grad_dtype == "f32":
             mix = stream_mix_ceilings(zo, torch, state, g, gb, d, mode)
+        pattern = server_pattern(zo, torch, wl, state, packed, W, nwords)
 
     ms_per_step = wall * 1000.0 / args.steps
     value = 2.0 * d / (ms_per_step / 1000.0)
@@ -731,6 +759,9 @@ def main():
                    "frac_of_copy": None if not extras else round(
                        bytes_[n] / 1e9 / (per_kernel[n] / 1000.0) / copy_gbs, 4)}
                for n in names}
+    if pattern is not None and "srv" in kernels:
+        # the server's algorithmic rate against its access pattern's
+        kernels["srv"]["frac_of_pattern"] = round(kernels["srv"]["gbs"] / pattern["gbs"], 4)
     dom = max(names, key=lambda n: per_kernel[n])
     step_bytes = sum(bytes_.values())
     tb = measured_traffic(dom, mode, wl.name)
@@ -764,6 +795,8 @@ def main():
         "inexact_chunks": inexact,
         "copy_gbs": round(copy_gbs, 1) if extras else None,
         "stream_mix_ceiling": mix,
+        # the single server's memory accesses without its arithmetic
+        "server_pattern": pattern,
         # the workload's own schedule once (mostly local steps after the warm-up phase)
         "schedule_run": sched,
         # the server at one GPU's share of a W-GPU sharded run, and that GPU's time for a

@@ -342,6 +342,18 @@ int zo_diag_copy(const float *src, float *dst, int64_t n, int nontemporal, hipSt
 int zo_diag_stream(const float *const *src, int32_t nsrc, float *const *dst, int32_t ndst,
                    int64_t n, hipStream_t stream);
 
+/* The memory accesses of zo_unpack_average's kernel without its arithmetic,
+ * on h's server range: per chunk one workgroup in the server's shape and
+ * order, each lane reading its packed dword of the chunk from all `world`
+ * rows of `packed` (laid out as for zo_unpack_average), then the chunk's
+ * server error (the srv_err buffer of h's state) loaded and stored back
+ * unchanged with the server's nontemporal accesses: the error keeps its
+ * bits.  Timing it measures the HBM rate the server's access pattern can
+ * reach.  Enqueued on h's stream; no state-machine effect (any phase).
+ * Chunks of at most 1024 elements (several chunks per workgroup) are not
+ * covered: ZO_EINVAL. */
+int zo_diag_server_pattern(zo_adam *h, const uint64_t *packed);
+
 /* ---- planning helpers (pure host; usable without a GPU) ----------------- */
 /* Validate a configuration exactly as zo_adam_init does. */
 int zo_config_check(const zo_config *cfg);

@@ -27,6 +27,7 @@ EXPORTS = (
     "zo_packed_words",
     "zo_server_range", "zo_chunk_table", "zo_gamma_sum", "zo_next_step", "zo_inexact_chunks",
     "zo_strerror", "zo_last_hip_error", "zo_diag_divsqrt", "zo_diag_copy", "zo_diag_stream",
+    "zo_diag_server_pattern",
     "zo_config_check", "zo_plan_num_chunks", "zo_plan_chunks",
 )
 
@@ -95,6 +96,7 @@ def lib():
             "zo_diag_divsqrt": ([vp, vp, vp, vp, i64, vp], ci),
             "zo_diag_copy": ([vp, vp, i64, ci, vp], ci),
             "zo_diag_stream": ([vp, i32, vp, i32, i64, vp], ci),
+            "zo_diag_server_pattern": ([vp, vp], ci),
             "zo_config_check": ([ctypes.POINTER(_Config)], ci),
             "zo_plan_num_chunks": ([i32, vp, i32], i64),
             "zo_plan_chunks": ([i32, vp, i32, vp, vp, vp], i64),
@@ -211,6 +213,10 @@ def zo_compress_pack_ef(h, t, gamma, g, packed0, scales0):
 def zo_unpack_average(h, t, packed, scales, srv_packed, srv_scales, avg_debug=None):
     _call(h, "zo_unpack_average", int(t), _ptr(packed), _ptr(scales), _ptr(srv_packed),
           _ptr(srv_scales), _ptr(avg_debug))
+
+
+def zo_diag_server_pattern(h, packed):
+    _call(h, "zo_diag_server_pattern", _ptr(packed))
 
 
 def zo_sync_update(h, t, srv_packed, srv_scales, gbar=None):
@@ -382,6 +388,13 @@ class ZoAdam:
             _need(packed0, "packed0", "int64", self.nwords)
             _need(scales0, "scales0", "float32", self.nchunks)
         zo_compress_pack_ef(self.h, t, gamma, g, packed0, scales0)
+
+    def diag_server_pattern(self, packed):
+        """The server's memory accesses without its arithmetic (the server
+        error is rewritten unchanged); see zo_diag_server_pattern."""
+        if self.r_chunks:
+            _need(packed, "packed", "int64", int(self.cfg["world"]) * self.r_words)
+        zo_diag_server_pattern(self.h, packed)
 
     def unpack_average(self, t, packed, scales, srv_packed, srv_scales, avg_debug=None):
         W = int(self.cfg["world"])

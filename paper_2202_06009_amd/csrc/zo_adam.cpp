@@ -612,6 +612,18 @@ int zo_diag_copy(const float *src, float *dst, int64_t n, int nontemporal, hipSt
     return e == hipSuccess ? ZO_OK : ZO_EHIP;
 }
 
+int zo_diag_server_pattern(zo_adam *h, const uint64_t *packed)
+{
+    if (!h) return ZO_EINVAL;
+    const int64_t nch = h->c1 - h->c0;
+    if (nch > 0 && !packed) return ZO_EINVAL;
+    if (!aligned(packed, 8)) return ZO_EALIGN;
+    if (h->chunk <= 1024) return ZO_EINVAL;  // the server's one-chunk-per-workgroup shapes
+    hipError_t e = zo::launch_srv_pattern(h->chunk, packed, h->world, h->w1 - h->w0, h->ch, h->c0,
+                                          nch, h->w0, h->e0, h->st.srv_err, h->stream);
+    return e == hipSuccess ? ZO_OK : h->hip_fail(e);
+}
+
 int zo_diag_stream(const float *const *src, int32_t nsrc, float *const *dst, int32_t ndst,
                    int64_t n, hipStream_t stream)
 {

@@ -108,6 +108,9 @@ struct StreamPtrs {
     float *dst[5];
 };
 hipError_t launch_stream(int R, int S, const StreamPtrs &p, int64_t n, hipStream_t st);
+hipError_t launch_srv_pattern(int chunk, const uint64_t *packed, int W, int64_t wstride,
+                              const Chunks &ch, int64_t c0, int64_t nch, int64_t word0,
+                              int64_t elem0, float *srv_err, hipStream_t st);
 hipError_t launch_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,
                           hipStream_t st);
 

@@ -1086,6 +1086,46 @@ __global__ __launch_bounds__(256) void k_stream(StreamPtrs p, int64_t n4)
     }
 }
 
+// The memory accesses of k_srv_lut without its arithmetic: per chunk of the
+// server range one workgroup of LD lanes in the same XCD-aware order, each lane
+// reading its dword of the chunk from all W workers' rows, then the chunk's
+// server error loaded and stored back unchanged with the kernel's nontemporal
+// accesses and float4 layout.  The error keeps its bits; timing it measures
+// the rate the server's access pattern can reach.
+template <int LD>
+__global__ __launch_bounds__(LD) void k_srv_pattern(const uint32_t *__restrict__ packed32, int W,
+                                                    int64_t wstride, Chunks ch, int64_t c0,
+                                                    int64_t nch, int64_t word0, int64_t elem0,
+                                                    float *__restrict__ srv_err)
+{
+    const int lc = (int)threadIdx.x;
+    const int64_t cr = xcd_block();
+    if (cr >= nch) return;
+    const int64_t c = c0 + cr;
+    const int len = ch.len[c];
+    const int64_t el = ch.start[c] - elem0;
+    const int64_t wd = ch.word[c] - word0;
+    uint32_t x = 0;
+    if (lc < (len + 31) >> 5) {
+        const uint32_t *p = packed32 + 2 * wd + lc;
+        const int64_t ws = 2 * wstride;
+#pragma unroll 8
+        for (int w = 0; w < W; ++w) x ^= p[ws * w];
+    }
+    asm volatile("" ::"v"(x));  // the loads are not dead
+    f4v v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const int e = 4 * LD * k + 4 * lc;
+        if (e < len) v[k] = ldnt(srv_err, (el + e) >> 2);
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const int e = 4 * LD * k + 4 * lc;
+        if (e < len) stnt(srv_err, (el + e) >> 2, v[k]);
+    }
+}
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
@@ -1484,6 +1524,25 @@ hipError_t launch_stream(int R, int S, const StreamPtrs &p, int64_t n, hipStream
     case 6: return stream_r<6>(S, p, n4, st);
     default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_srv_pattern(int chunk, const uint64_t *packed, int W, int64_t wstride,
+                              const Chunks &ch, int64_t c0, int64_t nch, int64_t word0,
+                              int64_t elem0, float *srv_err, hipStream_t st)
+{
+    const Geometry sg = srv_geometry_for(chunk);
+    if (sg.V != 1 || sg.L < 64) return hipErrorInvalidValue;
+    if (nch == 0) return hipSuccess;
+    const dim3 grid(xcd_grid(grid_for(nch, 1)));
+    const uint32_t *p = reinterpret_cast<const uint32_t *>(packed);
+    switch (sg.L) {
+    case 64: hipLaunchKernelGGL(k_srv_pattern<64>, grid, dim3(64), 0, st, p, W, wstride, ch, c0, nch, word0, elem0, srv_err); break;
+    case 128: hipLaunchKernelGGL(k_srv_pattern<128>, grid, dim3(128), 0, st, p, W, wstride, ch, c0, nch, word0, elem0, srv_err); break;
+    case 256: hipLaunchKernelGGL(k_srv_pattern<256>, grid, dim3(256), 0, st, p, W, wstride, ch, c0, nch, word0, elem0, srv_err); break;
+    case 512: hipLaunchKernelGGL(k_srv_pattern<512>, grid, dim3(512), 0, st, p, W, wstride, ch, c0, nch, word0, elem0, srv_err); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_copy(const float *src, float *dst, int64_t n, bool nt, hipStream_t st)

@@ -172,3 +172,6 @@ def test_unknown_algorithm_is_rejected():
 def test_fullprec_step_rejects_null_handle():
     assert zo.lib().zo_fullprec_step(None, 0, 1e-4, None) == zo.ZO_EINVAL
 
+
+def test_server_pattern_diagnostic_rejects_null_handle():
+    assert zo.lib().zo_diag_server_pattern(None, None) == zo.ZO_EINVAL

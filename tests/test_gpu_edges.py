@@ -331,3 +331,41 @@ def test_diag_stream_mix(torch_cuda):
     for w in range(5):
         ref = (acc + np.float32(w)).astype(np.float32)
         assert np.array_equal(dst[w].cpu().numpy(), ref), w
+
+
+def test_server_pattern_diagnostic_keeps_the_error(torch_cuda):
+    """zo_diag_server_pattern (the server's accesses without its arithmetic)
+    rewrites the server error with exactly the bits it held, including -0 and
+    a NaN payload, on a ragged layout; chunks of at most 1024 elements are
+    rejected."""
+    import paper_2202_06009_amd as zo
+    torch = torch_cuda
+    dev = torch.device("cuda", 0)
+    seg = C.offsets([5000, 3 * 2048 + 100, 12])
+    d, W = seg[-1], 5
+    state = {k: torch.zeros(d, dtype=torch.float32, device=dev)
+             for k in ("x", "m", "v", "u", "err", "srv_err", "anchor")}
+    opt = zo.ZoAdam(beta1=0.9, beta2=0.999, eps=1e-8, world=W, chunk=2048, seg_off=seg,
+                    tv=[], tu=[0], state=state)
+    try:
+        rng = np.random.default_rng(7)
+        bits = rng.integers(0, 2**32, size=d, dtype=np.uint64).astype(np.uint32)
+        bits[:8] = [0x80000000, 0x7fc01234, 0xff800000, 0, 1, 0x80000001, 0x3f800000, 0xbf800000]
+        state["srv_err"].copy_(torch.from_numpy(bits.view(np.int32)).to(dev).view(torch.float32))
+        before = state["srv_err"].view(torch.int32).clone()
+        packed = torch.from_numpy(rng.integers(-2**62, 2**62, size=(W, opt.nwords),
+                                               dtype=np.int64)).to(dev)
+        opt.diag_server_pattern(packed)
+        torch.cuda.synchronize()
+        assert torch.equal(state["srv_err"].view(torch.int32), before)
+    finally:
+        opt.close()
+    narrow = zo.ZoAdam(beta1=0.9, beta2=0.999, eps=1e-8, world=W, chunk=1024, seg_off=seg,
+                       tv=[], tu=[0], state=state)
+    try:
+        with pytest.raises(zo.ZoError) as e:
+            narrow.diag_server_pattern(
+                torch.zeros((W, narrow.nwords), dtype=torch.int64, device=dev))
+        assert e.value.status == zo.ZO_EINVAL
+    finally:
+        narrow.close()
