@@ -722,12 +722,22 @@ __device__ __forceinline__ int xpose_slot(int t)
 // chunks per workgroup.  The tables of chunk q of the workgroup start at byte
 // q*G*2048 of `tab` (with half tables, q*G*256 of `half`); with one chunk per
 // workgroup the offset of every lookup is an immediate.  With half tables the
-// LDS leaves room for four one-wave workgroups per SIMD: the register budget
-// is held to that (at 1024-element chunks and W = 32, a 20-byte spill; 74
-// instead of 81 us on the ResNet-50 shape).
+// register budget is held to the waves per SIMD that the workgroups' LDS
+// allows, at most four (at 1024-element chunks and W = 32: four, with a
+// 20-byte spill; 74 instead of 81 us on the ResNet-50 shape).
+constexpr int srv_lut_waves(int LD, int G)
+{
+    if (!srv_nibble(LD)) return 1;  // no bound beyond the workgroup size
+    const int cpw = srv_chunks_per_block(LD, G);
+    const int lds = cpw * LD * 128 + cpw * G * (256 + 32) + 256;  // transpose, tables, scales, tree
+    const int per_cu = 160 * 1024 / lds;                         // one-wave workgroups per CU
+    const int per_simd = (per_cu + 3) / 4;
+    return per_simd < 1 ? 1 : (per_simd > 4 ? 4 : per_simd);
+}
+
 template <int LD, int G>
 __global__ __launch_bounds__(LD > 64 ? LD : 64)
-__attribute__((amdgpu_waves_per_eu(srv_nibble(LD) ? 4 : 1))) void k_srv_lut(
+__attribute__((amdgpu_waves_per_eu(srv_lut_waves(LD, G)))) void k_srv_lut(
     const uint32_t *__restrict__ packed32, const float *__restrict__ scales, int W,
     int64_t wstride, int64_t cstride, Chunks ch, int64_t c0, int64_t nch, int64_t word0,
     int64_t elem0, float *__restrict__ srv_err, uint32_t *__restrict__ srv_packed32,
