@@ -26,6 +26,12 @@
  *     enqueues one and zo_materialize up to three elementwise kernels.
  *     Device faults surface at the caller's synchronisation.
  *   - No entry point after zo_adam_init allocates memory.
+ *   - The hot-path calls may be recorded into a HIP graph (stream capture):
+ *     each enqueues one kernel and no memset or copy.  A replay repeats the
+ *     recorded arguments (step scalars, the implicit-state modes of deferred
+ *     writes), so it stands for later steps only where those repeat, e.g. a
+ *     steady local/sync alternation at a constant learning rate; the host's
+ *     step counter does not advance on replays.
  *   - A handle is not thread-safe; use one handle per stream.
  *   - Arithmetic is IEEE binary32 with one rounding per operation, no FMA
  *     contraction, correctly rounded division and square root, no flushing of

@@ -1,0 +1,97 @@
+"""The hot path under HIP graph capture: every hot-path call enqueues one
+kernel and allocates nothing, so a steady-state step pair (a local+variance
+step, then a sync+variance step with deferred writes) captured once replays
+as often as wanted.  Each replay is checked, bit for bit and over every
+buffer the path writes, against the same steps run eagerly on a twin handle
+in lockstep."""
+import numpy as np
+import pytest
+
+from synth import configs as C
+
+pytestmark = pytest.mark.gpu
+
+KEYS = ("x", "m", "v", "u", "err", "srv_err", "anchor")
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+class Twin:
+    """One worker's handle with its own buffers, fed the inputs given."""
+
+    def __init__(self, torch, zo, seg, W, chunk, T, x0, g, gb, peers, peer_scales):
+        d = seg[-1]
+        self.state = {k: torch.zeros(d, dtype=torch.float32, device="cuda") for k in KEYS}
+        self.state["x"].copy_(x0)
+        self.g, self.gb = g.clone(), gb.clone()
+        self.opt = zo.ZoAdam(beta1=0.9, beta2=0.999, eps=1e-8, world=W, chunk=chunk,
+                             seg_off=seg, tv=list(range(T)), tu=list(range(1, T, 2)),
+                             state=self.state, defer_sync_writes=True)
+        self.packed = torch.zeros((W, self.opt.nwords), dtype=torch.int64, device="cuda")
+        self.scales = torch.zeros((W, self.opt.nchunks), dtype=torch.float32, device="cuda")
+        self.packed[1:] = peers
+        self.scales[1:] = peer_scales
+        self.srv_packed = torch.zeros(self.opt.nwords, dtype=torch.int64, device="cuda")
+        self.srv_scales = torch.zeros(self.opt.nchunks, dtype=torch.float32, device="cuda")
+
+    def pair(self, t):
+        """Steps t (local + variance) and t + 1 (sync + variance), t even."""
+        o, gam = self.opt, 1e-4
+        o.local_step(t, gam, self.g, self.gb)
+        o.compress_pack_ef(t + 1, gam, self.g, self.packed[0], self.scales[0])
+        o.unpack_average(t + 1, self.packed, self.scales, self.srv_packed, self.srv_scales)
+        o.sync_update(t + 1, self.srv_packed, self.srv_scales, self.gb)
+
+    def buffers(self):
+        return [self.state[k] for k in KEYS] + [self.packed[0], self.scales[0],
+                                                self.srv_packed, self.srv_scales]
+
+
+def _bits(t):
+    return t.cpu().numpy().view(np.uint32 if t.element_size() == 4 else np.uint64)
+
+
+def test_captured_step_pair_replays_bit_exactly(torch_cuda):
+    import paper_2202_06009_amd as zo
+    torch = torch_cuda
+    seg = C.offsets([5000, 3 * 2048 + 100, 12])
+    d, W, chunk, replays = seg[-1], 4, 2048, 4
+    T = 2 + 2 * replays
+    gen = torch.Generator(device="cuda").manual_seed(11)
+    x0 = torch.randn(d, device="cuda", generator=gen) * 0.02
+    g = torch.randn(d, device="cuda", generator=gen) * 1e-3
+    gb = torch.randn(d, device="cuda", generator=gen) * 1e-3
+    nwords = zo.zo_plan_chunks(seg, chunk)[3]
+    nch = len(zo.zo_plan_chunks(seg, chunk)[1])
+    peers = torch.randint(-2**62, 2**62, (W - 1, nwords), device="cuda", generator=gen)
+    peer_scales = 2.0e-8 * (1.0 + 0.5 * torch.rand((W - 1, nch), device="cuda", generator=gen))
+    eager = Twin(torch, zo, seg, W, chunk, T, x0, g, gb, peers, peer_scales)
+    graphed = Twin(torch, zo, seg, W, chunk, T, x0, g, gb, peers, peer_scales)
+    try:
+        # the first pair eagerly on both: it leaves the deferred-write state
+        # (model in the anchor, buffer implicit) that every later pair starts from
+        eager.pair(0)
+        graphed.pair(0)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            graphed.opt.set_stream(None)      # the capture stream
+            graphed.pair(2)
+        graphed.opt.set_stream(None)          # back to the default stream
+        for r in range(replays):
+            graph.replay()
+            eager.pair(2 + 2 * r)
+            torch.cuda.synchronize()
+            for k, (a, b) in enumerate(zip(eager.buffers(), graphed.buffers())):
+                ua, ub = _bits(a), _bits(b)
+                assert np.array_equal(ua, ub), (r, k, int(np.sum(ua != ub)))
+        assert eager.opt.inexact_chunks() == 0
+    finally:
+        eager.opt.close()
+        graphed.opt.close()
