@@ -305,6 +305,48 @@ def stream_mix_ceilings(zo, torch, state, g, gb, d, mode):
     return out
 
 
+def graph_replay(zo, torch, wl, state, g_in, gb_in, packed, scales, srv_packed, srv_scales,
+                 deferred, grad_dtype, replays):
+    """The bench step (local+variance, then sync+variance) recorded once in a
+    HIP graph after one eager step pair, then replayed `replays` times: the
+    step's time without host launch overhead.  Each replay repeats the
+    recorded step (constant learning rate, the same inputs), as the timed
+    region does."""
+    d = wl.n
+    T = 4
+    opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=wl.world, chunk=wl.chunk,
+                    seg_off=wl.seg_off, tv=list(range(T)), tu=list(range(1, T, 2)),
+                    state=state, defer_sync_writes=deferred, grad_dtype=grad_dtype)
+    gamma = 1e-4
+
+    def pair(t):
+        opt.local_step(t, gamma, g_in, gb_in)
+        opt.compress_pack_ef(t + 1, gamma, g_in, packed[0], scales[0])
+        opt.unpack_average(t + 1, packed, scales, srv_packed, srv_scales)
+        opt.sync_update(t + 1, srv_packed, srv_scales, gb_in)
+
+    pair(0)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        opt.set_stream(None)  # the capture stream
+        pair(2)
+    opt.set_stream(None)
+    graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(replays):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / replays
+    opt.close()
+    del graph
+    return {"replays": replays, "ms_per_step": round(ms, 4),
+            "params_per_s": round(2.0 * d / (ms / 1000.0), 1)}
+
+
 def server_pattern(zo, torch, wl, state, packed, W, nwords, reps=4):
     """The server's access pattern without its arithmetic (zo_diag_server_pattern
     on a handle over the whole shard, best of the last reps-1 launches): the
@@ -722,13 +764,16 @@ def main():
     # schedule run launch the same kernels at other sizes, the ceiling the
     # same copy kernel).
     extras = not args.copy_calibration
-    share = sched = mix = pattern = None
+    share = sched = mix = pattern = graphed = None
     copy_gbs = float("nan")
     if extras and not fv:
         share = server_share(zo, torch, wl, state, g_in, packed, scales, srv_packed, srv_scales,
                              W)
         sched = schedule_run(zo, torch, wl, state, g_in, gb_in, packed, scales, srv_packed,
                              srv_scales, not args.eager_sync_writes, args.grad_dtype)
+        graphed = graph_replay(zo, torch, wl, state, g_in, gb_in, packed, scales, srv_packed,
+                               srv_scales, not args.eager_sync_writes, args.grad_dtype,
+                               args.steps)
     if extras:
         # the practical ceiling: a plain copy of one state vector (best of three)
         copy_ms = []
@@ -797,6 +842,8 @@ def main():
         "stream_mix_ceiling": mix,
         # the single server's memory accesses without its arithmetic
         "server_pattern": pattern,
+        # the same bench step recorded once in a HIP graph and replayed
+        "graph_replay": graphed,
         # the workload's own schedule once (mostly local steps after the warm-up phase)
         "schedule_run": sched,
         # the server at one GPU's share of a W-GPU sharded run, and that GPU's time for a
