@@ -645,8 +645,8 @@ def main():
         summarize_trace(args.summarize_trace, mode, args.workload, args.warmup, args.steps)
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: the multi-GPU exchange of the method is not "
-              f"part of this build (asked for --gpus {args.gpus})", file=sys.stderr)
+        print(f"bench.py runs on one GPU only: the library is one worker's step on one GPU and "
+              f"implements no multi-GPU exchange (asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
 
     from synth import configs as C
