@@ -155,6 +155,65 @@ def summarize_trace(trace_dir, mode, workload, warmup, steps):
               f"{model[key] / 1e9:.3f} | {gbs:.0f} | {100 * gbs / HBM_PEAK_GBS:.1f} |")
 
 
+def variant_of_kernel(name):
+    """(variant, bytes per gradient element) of an Algorithm 1 kernel's
+    template name, or None: the inverse of VARIANT_KERNELS."""
+    m = re.match(r"zo::k_local<(true|false), (\d), (true|false), (\d)>", name)
+    if m:
+        base = {"0": "local", "1": "local (u=0)", "2": "local (u=gm)"}[m.group(2)]
+        return base + ("+var" if m.group(1) == "true" else ""), (4, 2, 2)[int(m.group(4))]
+    m = re.match(r"zo::k_sync1<\d+, \d+, true, (\d), (\d)>", name)
+    if m:
+        base = {"0": "sync1", "1": "sync1 (u=0)", "2": "sync1 (u=gm)"}[m.group(1)]
+        return base, (4, 2, 2)[int(m.group(2))]
+    if re.match(r"zo::k_srv_(lut|plain)<", name):
+        return "srv", 4
+    m = re.match(r"zo::k_recon<(true|false), (true|false), (\d)>", name)
+    if m:
+        base = "recon (deferred)" if m.group(2) == "true" else "recon"
+        return base + ("+var" if m.group(1) == "true" else ""), (4, 2, 2)[int(m.group(3))]
+    return None
+
+
+def summarize_kernels(trace_dir, workload):
+    """Every kernel of a `rocprofv3 --kernel-trace` run grouped by template
+    name and grid size, with the algorithmic bytes of the Algorithm 1 variants
+    at their largest grid for the name (the whole shard of `workload`; smaller
+    grids are other sizes, e.g. the server share).  Prints a markdown table."""
+    import statistics
+    import paper_2202_06009_amd as zo
+    from synth import configs as C
+    rows = []
+    for root, _, files in os.walk(trace_dir):
+        for fn in files:
+            if fn.endswith("kernel_trace.csv"):
+                rows += list(csv.DictReader(open(os.path.join(root, fn))))
+    wl = C.get(workload)
+    _, ln, _, nwords = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
+    groups = {}
+    for r in rows:
+        name = r["Kernel_Name"].replace("void ", "").split("(")[0]
+        grid = int(r.get("Grid_Size_X") or r.get("Grid_Size") or 0)
+        us = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0
+        groups.setdefault((name, grid), []).append(us)
+    biggest = {}
+    for name, grid in groups:
+        biggest[name] = max(grid, biggest.get(name, 0))
+    print("| kernel | grid | calls | avg µs | median µs | variant | algorithmic GB/launch "
+          "| GB/s | % of 8 TB/s |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for (name, grid), us in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        avg = sum(us) / len(us)
+        v = variant_of_kernel(name)
+        cols = ["", "", "", ""]
+        if v is not None and grid == biggest[name]:
+            nb = variant_bytes(v[0], wl.n, len(ln), nwords, wl.world, v[1])
+            gbs = nb / 1e9 / (avg / 1e6)
+            cols = [v[0], f"{nb / 1e9:.3f}", f"{gbs:.0f}", f"{100 * gbs / HBM_PEAK_GBS:.1f}"]
+        print(f"| `{name}` | {grid} | {len(us)} | {avg:.1f} | {statistics.median(us):.1f} | "
+              + " | ".join(cols) + " |")
+
+
 def summarize_pmc(fetch_dir, write_dir, out_path, mode, workload):
     """Turn two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) over
     `bench.py --copy-calibration` into per-launch HBM traffic, each counter
@@ -230,6 +289,57 @@ def algorithmic_bytes_fv(d, nchunks, nwords, W, gbytes=4):
     }
 
 
+# Kernel variants of Algorithm 1 (zo_local_step, zo_compress_pack_ef,
+# zo_unpack_average, zo_sync_update) by where u is before the call, and the
+# kernel template each launches (GT = gradient type).  "(u=0)": the first call
+# after a deferred sync (u = +0, m from the 1-bit copy of the server output);
+# "(u=gm)": u = +0 + gamma m left implicit by that first local step.
+VARIANT_KERNELS = {
+    "local": "k_local<{var}, 0, true, {gt}>",
+    "local (u=0)": "k_local<{var}, 1, false, {gt}>",
+    "local (u=gm)": "k_local<{var}, 2, true, {gt}>",
+    "sync1": "k_sync1<L, V, true, 0, {gt}>",
+    "sync1 (u=0)": "k_sync1<L, V, true, 1, {gt}>",
+    "sync1 (u=gm)": "k_sync1<L, V, true, 2, {gt}>",
+    "srv": "k_srv_lut<LD, G>",
+    "recon": "k_recon<{var}, false, {gt}>",
+    "recon (deferred)": "k_recon<{var}, true, {gt}>",
+}
+
+
+def variant_bytes(name, d, nchunks, nwords, W, gbytes=4):
+    """Algorithmic bytes per launch of a kernel variant of Algorithm 1: every
+    array it must read and write once, packed words (8 per word) and one
+    binary32 scale per chunk included; a name ending in "+var" has the
+    variance line fused (gbar read, v written).  gbytes: bytes per element of
+    g and gbar."""
+    cp = 8 * nwords + 4 * nchunks          # one packed buffer: words and scales
+    var = name.endswith("+var")
+    base = name[:-4] if var else name
+    table = {
+        # reads g, m, x, v, u; writes m, x, u
+        "local": (28 + gbytes) * d,
+        # reads g, the server copy, the anchor, v; writes m, x
+        "local (u=0)": (16 + gbytes) * d + cp,
+        # reads g, m, x, v; writes m, x, u
+        "local (u=gm)": (24 + gbytes) * d,
+        # reads g, m, u, err; writes err, own words and scales
+        "sync1": (16 + gbytes) * d + cp,
+        # reads g, m, err; writes err, own words and scales
+        "sync1 (u=gm)": (12 + gbytes) * d + cp,
+        # reads g, the server copy, err; writes err, own words and scales
+        "sync1 (u=0)": (8 + gbytes) * d + 2 * cp,
+        # reads W packed buffers and the server error; writes the server error
+        # and the server words and scales
+        "srv": W * cp + 8 * d + cp,
+        # reads server words and scales, v, anchor; writes m, x, anchor, u
+        "recon": 24 * d + cp,
+        # reads server words and scales, v, anchor; writes anchor and the copy
+        "recon (deferred)": 12 * d + 2 * cp,
+    }
+    return table[base] + ((gbytes + 4) * d if var else 0)
+
+
 def algorithmic_bytes(d, nchunks, nwords, W, deferred=True, gbytes=4):
     """Bytes each kernel must move per launch: every state read once and
     written once, packed words and per-chunk scales included (gbytes: bytes
@@ -238,23 +348,11 @@ def algorithmic_bytes(d, nchunks, nwords, W, deferred=True, gbytes=4):
     words and scales; the local step after it reads x from the anchor and m
     from that copy, and neither reads nor writes u (u = +0 + gamma m there);
     the compress that follows forms u from the m it reads."""
-    pk = 8 * nwords
-    sc = 4 * nchunks
-    return {
-        # reads g, gbar, x, v, m (eager; deferred: the server copy), u (eager);
-        # writes m, x, v, u (eager only)
-        "local+var": (32 + 2 * gbytes) * d if not deferred else
-                     (20 + 2 * gbytes) * d + pk + sc,
-        # reads g, m, err, u (eager only); writes err, own packed words, own scales
-        "sync1": ((12 if deferred else 16) + gbytes) * d + pk + sc,
-        # reads W packed buffers + W scale rows + server error;
-        # writes server error, server packed words, server scales
-        "srv": W * (pk + sc) + 8 * d + pk + sc,
-        # reads server words + scales, v, anchor, gbar; writes anchor, v, and
-        # m, x, u (eager) or the copy of the server words + scales (deferred)
-        "recon+var": pk + sc + (28 + gbytes) * d if not deferred else
-                     2 * (pk + sc) + (16 + gbytes) * d,
-    }
+    v = {"local+var": "local (u=0)+var" if deferred else "local+var",
+         "sync1": "sync1 (u=gm)" if deferred else "sync1",
+         "srv": "srv",
+         "recon+var": "recon (deferred)+var" if deferred else "recon+var"}
+    return {k: variant_bytes(name, d, nchunks, nwords, W, gbytes) for k, name in v.items()}
 
 
 def stream_mix_ceilings(zo, torch, state, g, gb, d, mode):
@@ -425,38 +523,144 @@ def schedule_run(zo, torch, wl, state, g_in, gb_in, packed, scales, srv_packed, 
     learning rates): sync steps while the variance is updated, then local
     steps between ever rarer syncs.  Timed with HIP events around the whole
     run (after one untimed run of the same schedule on another handle);
-    run-level params/s = d * steps / time.  Inputs are the bench's buffers,
-    reused at every step."""
+    run-level params/s = d * steps / time.  Every launch is also bracketed by
+    events of its own and sorted into the kernel variant it ran (by where u
+    was before the call), so `kernels` holds, per variant, the launches, their
+    average time and the algorithmic rate against 8 TB/s.  Inputs are the
+    bench's buffers, reused at every step."""
     tu, tv = set(wl.tu), set(wl.tv)
+    _, ln, _, nwords = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
+    gbytes = g_in.element_size()
+    gt = {4: 0, 2: 1 if g_in.dtype == torch.float16 else 2}[gbytes]
 
     def run(timed):
         opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=wl.world,
                         chunk=wl.chunk, seg_off=wl.seg_off, tv=wl.tv, tu=wl.tu, state=state,
                         defer_sync_writes=deferred, grad_dtype=grad_dtype)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        marks = []
+
+        def call(name, f):
+            if timed:
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                f()
+                b.record()
+                marks.append((name, a, b))
+            else:
+                f()
         try:
             torch.cuda.synchronize()
             e0.record()
             for t in range(wl.steps):
                 gam, gb = wl.gamma(t), (gb_in if t in tv else None)
+                vs = "+var" if gb is not None else ""
+                umode = zo.zo_state_location(opt.h)[1]
+                u = {zo.U_IN_BUFFER: "", zo.U_ZERO: " (u=0)", zo.U_GAMMA_M: " (u=gm)"}[umode]
                 if t in tu:
-                    opt.compress_pack_ef(t, gam, g_in, packed[0], scales[0])
-                    opt.unpack_average(t, packed, scales, srv_packed, srv_scales)
-                    opt.sync_update(t, srv_packed, srv_scales, gb)
+                    call("sync1" + u, lambda: opt.compress_pack_ef(t, gam, g_in, packed[0],
+                                                                   scales[0]))
+                    call("srv", lambda: opt.unpack_average(t, packed, scales, srv_packed,
+                                                           srv_scales))
+                    call(("recon (deferred)" if deferred else "recon") + vs,
+                         lambda: opt.sync_update(t, srv_packed, srv_scales, gb))
                 else:
-                    opt.local_step(t, gam, g_in, gb)
+                    call("local" + u + vs, lambda: opt.local_step(t, gam, g_in, gb))
             e1.record()
             torch.cuda.synchronize()
         finally:
             opt.close()
-        return e0.elapsed_time(e1)
+        return e0.elapsed_time(e1), marks
 
     run(False)
-    ms = run(True)
+    ms, marks = run(True)
+    per = {}
+    for name, a, b in marks:
+        per.setdefault(name, []).append(a.elapsed_time(b))
+    kernels = {}
+    total_bytes = 0.0
+    for name, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
+        avg = sum(v) / len(v)
+        nb = variant_bytes(name, wl.n, len(ln), nwords, wl.world, gbytes)
+        total_bytes += nb * len(v)
+        base = name[:-4] if name.endswith("+var") else name
+        kernels[name] = {
+            "kernel": VARIANT_KERNELS[base].format(var="true" if name.endswith("+var")
+                                                   else "false", gt=gt),
+            "launches": len(v), "ms": round(avg, 4), "ms_total": round(sum(v), 3),
+            "gb_per_launch": round(nb / 1e9, 3),
+            "gbs": round(nb / 1e9 / (avg / 1000.0), 1),
+            "frac": round(nb / 1e9 / (avg / 1000.0) / HBM_PEAK_GBS, 4)}
     return {"steps": wl.steps, "syncs": len(tu), "variance_updates": len(tv),
             "local_steps": wl.steps - len(tu), "ms": round(ms, 3),
             "ms_per_step": round(ms / wl.steps, 4),
-            "params_per_s": round(wl.n * wl.steps / (ms / 1000.0), 1)}
+            "params_per_s": round(wl.n * wl.steps / (ms / 1000.0), 1),
+            # every launch's algorithmic bytes over the run's time
+            "hbm_frac": round(total_bytes / 1e9 / (ms / 1000.0) / HBM_PEAK_GBS, 4),
+            "kernels": kernels}
+
+
+def general_kernels(zo, torch, wl, state, g_in, gb_in, packed, scales, srv_packed, srv_scales,
+                    grad_dtype, reps):
+    """Each step of the path in its general form, every state read and written
+    once (eager sync writes, u in its buffer): the local step with and
+    without the variance line, the fused compress, and the reconstruction
+    with and without the variance line, each launched `reps` times after two
+    untimed launches and timed with HIP events; algorithmic bytes by
+    variant_bytes.  Run A: local steps only, the variance line every other
+    step; run B: a sync at every step, the variance line every other step."""
+    _, ln, _, nwords = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
+    gbytes = g_in.element_size()
+    T = 2 * (reps + 2)
+    times = {}
+
+    def timed(name, t, f):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        f()
+        b.record()
+        if t >= 4:
+            times.setdefault(name, []).append((a, b))
+
+    gam = 1e-4
+    opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=wl.world, chunk=wl.chunk,
+                    seg_off=wl.seg_off, tv=list(range(0, T, 2)), tu=[], state=state,
+                    grad_dtype=grad_dtype)
+    try:
+        for t in range(T):
+            gb = gb_in if t % 2 == 0 else None
+            timed("local+var" if gb is not None else "local", t,
+                  lambda: opt.local_step(t, gam, g_in, gb))
+        torch.cuda.synchronize()
+    finally:
+        opt.close()
+    opt = zo.ZoAdam(beta1=wl.beta1, beta2=wl.beta2, eps=wl.eps, world=wl.world, chunk=wl.chunk,
+                    seg_off=wl.seg_off, tv=list(range(0, T, 2)), tu=list(range(T)), state=state,
+                    grad_dtype=grad_dtype)
+    try:
+        for t in range(T):
+            gb = gb_in if t % 2 == 0 else None
+            timed("sync1", t, lambda: opt.compress_pack_ef(t, gam, g_in, packed[0], scales[0]))
+            opt.unpack_average(t, packed, scales, srv_packed, srv_scales)
+            timed("recon+var" if gb is not None else "recon", t,
+                  lambda: opt.sync_update(t, srv_packed, srv_scales, gb))
+        torch.cuda.synchronize()
+    finally:
+        opt.close()
+    out = {}
+    for name in ("local", "local+var", "sync1", "recon", "recon+var"):
+        v = [a.elapsed_time(b) for a, b in times[name]]
+        avg = sum(v) / len(v)
+        nb = variant_bytes(name, wl.n, len(ln), nwords, wl.world, gbytes)
+        base = name[:-4] if name.endswith("+var") else name
+        out[name] = {"kernel": VARIANT_KERNELS[base].format(
+                         var="true" if name.endswith("+var") else "false",
+                         gt={4: 0, 2: 1 if g_in.dtype == torch.float16 else 2}[gbytes]),
+                     "launches": len(v), "ms": round(avg, 4),
+                     "gb_per_launch": round(nb / 1e9, 3),
+                     "gbs": round(nb / 1e9 / (avg / 1000.0), 1),
+                     "frac": round(nb / 1e9 / (avg / 1000.0) / HBM_PEAK_GBS, 4)}
+    return out
 
 
 def _oracle_share(wl, c0, c1, fv, barrier, results):
@@ -627,6 +831,9 @@ def main():
     ap.add_argument("--summarize-trace", metavar="TRACE_DIR",
                     help="print the timed kernels' durations from a rocprofv3 --kernel-trace "
                          "run of this command (same --workload/--warmup/--steps) and exit")
+    ap.add_argument("--summarize-kernels", metavar="TRACE_DIR",
+                    help="print every kernel of a rocprofv3 --kernel-trace run of this "
+                         "command, grouped by template and grid, and exit")
     ap.add_argument("--summarize-counters", nargs="+", metavar="PMC_DIR",
                     help="print the timed kernels' counters from rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
@@ -640,6 +847,9 @@ def main():
         return
     if args.summarize_counters:
         summarize_counters(args.summarize_counters, mode)
+        return
+    if args.summarize_kernels:
+        summarize_kernels(args.summarize_kernels, args.workload)
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace, mode, args.workload, args.warmup, args.steps)
@@ -764,13 +974,15 @@ def main():
     # schedule run launch the same kernels at other sizes, the ceiling the
     # same copy kernel).
     extras = not args.copy_calibration
-    share = sched = mix = pattern = graphed = None
+    share = sched = mix = pattern = graphed = general = None
     copy_gbs = float("nan")
     if extras and not fv:
         share = server_share(zo, torch, wl, state, g_in, packed, scales, srv_packed, srv_scales,
                              W)
         sched = schedule_run(zo, torch, wl, state, g_in, gb_in, packed, scales, srv_packed,
                              srv_scales, not args.eager_sync_writes, args.grad_dtype)
+        general = general_kernels(zo, torch, wl, state, g_in, gb_in, packed, scales, srv_packed,
+                                  srv_scales, args.grad_dtype, args.steps)
     if extras:
         # the practical ceiling: a plain copy of one state vector (best of three)
         copy_ms = []
@@ -860,10 +1072,23 @@ def main():
         "env": {"device": props.name, "arch": getattr(props, "gcnArchName", None),
                 "compute_units": props.multi_processor_count, "hip": torch.version.hip,
                 "torch": torch.__version__},
+        # each step of the path in its general form (every state read and written)
+        "general_kernels": general,
         "roofline": {"bound": "hbm", "kernel": dom,
                      "achieved": kernels[dom]["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": kernels[dom]["frac"], "traffic": traffic_gb},
+                     "frac": kernels[dom]["frac"], "traffic": traffic_gb,
+                     "gb_per_launch": kernels[dom]["gb_per_launch"]},
     }
+    if general is not None and dom in general:
+        # the same row with every state read and written (no deferred writes)
+        out["roofline"]["general_form"] = {k: general[dom][k] for k in (
+            "kernel", "gb_per_launch", "gbs", "frac")}
+    if sched is not None and sched.get("kernels"):
+        top = next(iter(sched["kernels"]))  # the variant with the most time in the schedule
+        out["roofline"]["schedule_dominant"] = {"variant": top} | {
+            k: sched["kernels"][top][k] for k in ("kernel", "launches", "ms_total",
+                                                 "gb_per_launch", "gbs", "frac")}
+        out["roofline"]["schedule_hbm_frac"] = sched["hbm_frac"]
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_chunks, fv)

@@ -36,8 +36,10 @@
  *   - Arithmetic is IEEE binary32 with one rounding per operation, no FMA
  *     contraction, correctly rounded division and square root, no flushing of
  *     denormals; the per-chunk L1 norm is the balanced pairwise tree over the
- *     chunk in index order; the server's average over workers is an exact sum
- *     (binary64) divided by W and rounded once to binary32.
+ *     chunk in index order; the server's average over workers is the exact
+ *     binary64 sum S divided by W in binary64 and rounded to binary32, which
+ *     is RN32(S / W): for a binary64 S and an integer W the intermediate
+ *     binary64 quotient never lands on a binary32 midpoint unless S / W does.
  *
  * Layout
  *   - The shard is a list of segments (one per parameter tensor); every
@@ -319,7 +321,8 @@ int zo_chunk_table(const zo_adam *h, int64_t *start, int64_t *len, int64_t *word
 float zo_gamma_sum(const zo_adam *h);
 int64_t zo_next_step(const zo_adam *h);
 /* Number of server-range chunks whose scales broke the exact-sum condition
- * in the most recent zo_unpack_average (synchronises the stream). */
+ * in at least one zo_unpack_average since zo_adam_init (a chunk's flag is
+ * never cleared; synchronises the stream). */
 int zo_inexact_chunks(zo_adam *h, int64_t *count);
 const char *zo_strerror(int status);
 const char *zo_last_hip_error(const zo_adam *h);

@@ -535,8 +535,9 @@ __global__ __launch_bounds__(L > 256 ? L : 256) void k_srv_plain(
     }
     compress_chunk<L, V>(b, lc, len, active, srv_err, el,
                          srv_packed32 + 2 * (active ? ch.word[c] : 0), srv_scales + c, lds);
+    // sticky: a flag once set stays set until the handle is recreated
     const uint32_t f = inexact_flag<L>(scales + (active ? cr : 0), cstride, W, lc);
-    if (active && lc == 0) flags[cr] = (uint8_t)f;
+    if (active && lc == 0 && f) flags[cr] = 1;
 }
 
 // Server with a lookup table per group of 8 workers ("four Russians"): for a
@@ -877,8 +878,9 @@ __attribute__((amdgpu_waves_per_eu(srv_lut_waves(LD, G)))) void k_srv_lut(
         load_serr();
     }
     {
+        // sticky: a flag once set stays set until the handle is recreated
         const uint32_t f = inexact_flag<LD>(sc + q * W, 1, W, lc);
-        if (active && lc == 0) flags[cr] = (uint8_t)f;
+        if (active && lc == 0 && f) flags[cr] = 1;
     }
 
     // averages -> LDS, then back in the coalesced layout of the compress step

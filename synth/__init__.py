@@ -33,6 +33,12 @@ def lib():
         L.zs_fill_bits_host.restype = None
         L.zs_fill_scales_host.argtypes = [vp, i64, i64, u64, f32]
         L.zs_fill_scales_host.restype = None
+        L.zs_fill_normal_host_ranges.argtypes = [vp, i64, vp, vp, u64, f32, u32, f32]
+        L.zs_fill_normal_host_ranges.restype = None
+        L.zs_fill_bits_host_ranges.argtypes = [vp, i64, vp, vp, u64]
+        L.zs_fill_bits_host_ranges.restype = None
+        L.zs_fill_scales_host_ranges.argtypes = [vp, i64, vp, vp, u64, f32]
+        L.zs_fill_scales_host_ranges.restype = None
         L.zs_fill_normal_dev.argtypes = [vp, i64, i64, u64, f32, u32, f32, vp]
         L.zs_fill_normal_dev.restype = ctypes.c_int
         L.zs_fill_bits_dev.argtypes = [vp, i64, i64, u64, vp]
@@ -64,6 +70,39 @@ def bits_host(nwords, word0, k):
 def scales_host(n, idx0, k, base):
     out = np.empty(int(n), np.float32)
     lib().zs_fill_scales_host(out.ctypes.data, int(n), int(idx0), k, float(base))
+    return out
+
+
+def _ranges(starts, lens):
+    s = np.ascontiguousarray(starts, dtype=np.int64)
+    n = np.ascontiguousarray(lens, dtype=np.int64)
+    assert s.shape == n.shape
+    return s, n, int(n.sum())
+
+
+def normal_host_ranges(starts, lens, k, ksig, per_mille=0, factor=1.0):
+    """normal_host over several index ranges, concatenated."""
+    s, n, tot = _ranges(starts, lens)
+    out = np.empty(tot, np.float32)
+    lib().zs_fill_normal_host_ranges(out.ctypes.data, len(s), s.ctypes.data, n.ctypes.data, k,
+                                     float(ksig), int(per_mille), float(factor))
+    return out
+
+
+def bits_host_ranges(word0s, nwords, k):
+    """bits_host over several word ranges, concatenated."""
+    s, n, tot = _ranges(word0s, nwords)
+    out = np.empty(tot, np.uint64)
+    lib().zs_fill_bits_host_ranges(out.ctypes.data, len(s), s.ctypes.data, n.ctypes.data, k)
+    return out
+
+
+def scales_host_ranges(starts, lens, k, base):
+    """scales_host over several index ranges, concatenated."""
+    s, n, tot = _ranges(starts, lens)
+    out = np.empty(tot, np.float32)
+    lib().zs_fill_scales_host_ranges(out.ctypes.data, len(s), s.ctypes.data, n.ctypes.data, k,
+                                     float(base))
     return out
 
 

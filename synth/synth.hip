@@ -85,6 +85,36 @@ void zs_fill_scales_host(float *out, int64_t n, int64_t idx0, uint64_t key, floa
     for (int64_t i = 0; i < n; ++i) out[i] = zs_scale(key, (uint64_t)(idx0 + i), base);
 }
 
+// The same fills over several index ranges [idx0[r], idx0[r] + len[r]), written
+// back to back into `out` (one call for a sample of scattered chunks).
+void zs_fill_normal_host_ranges(float *out, int64_t nranges, const int64_t *idx0,
+                                const int64_t *len, uint64_t key, float ksigma,
+                                uint32_t per_mille, float factor)
+{
+    for (int64_t r = 0; r < nranges; ++r) {
+        zs_fill_normal_host(out, len[r], idx0[r], key, ksigma, per_mille, factor);
+        out += len[r];
+    }
+}
+
+void zs_fill_bits_host_ranges(uint64_t *out, int64_t nranges, const int64_t *word0,
+                              const int64_t *nwords, uint64_t key)
+{
+    for (int64_t r = 0; r < nranges; ++r) {
+        zs_fill_bits_host(out, nwords[r], word0[r], key);
+        out += nwords[r];
+    }
+}
+
+void zs_fill_scales_host_ranges(float *out, int64_t nranges, const int64_t *idx0,
+                                const int64_t *len, uint64_t key, float base)
+{
+    for (int64_t r = 0; r < nranges; ++r) {
+        zs_fill_scales_host(out, len[r], idx0[r], key, base);
+        out += len[r];
+    }
+}
+
 }  // extern "C"
 
 // -------------------------------------------------------------- device fills

@@ -7,6 +7,8 @@ identical) for either the whole shard or a sample of chunks.  Every
 computation of the method is local to a chunk, so the oracle run on a sample
 of chunks reproduces exactly what a full run computes on those chunks.
 """
+import os
+
 import numpy as np
 
 import oracle as orc
@@ -41,45 +43,62 @@ def steps_kind(wl, t):
 # chunk sampling
 # ---------------------------------------------------------------------------
 
-def sample_chunks(lay, seg_off, budget_elems, stride_chunks=None):
-    """Chunks to check at scale: the first and the last chunk of segments
-    (every ragged tail is a last chunk), taken alternately from both ends of
-    the model until the element budget is spent, plus every
-    `stride_chunks`-th chunk."""
+def sample_chunks(lay, seg_off, stride=50, min_frac=0.02):
+    """Chunks to check at scale: every partial (ragged) chunk, the first and
+    the last chunk of every segment, and every `stride`-th of the remaining
+    chunks; the stride is lowered until the sample holds at least `min_frac`
+    of the shard's elements."""
     seg_off = np.asarray(seg_off, dtype=np.int64)
+    nch = lay.nchunks
+    if nch == 0:
+        return np.zeros(0, np.int64)
     seg = np.searchsorted(seg_off, lay.cstart, side="right") - 1
-    firsts = {}
-    lasts = {}
-    for c, sg in enumerate(seg):
-        firsts.setdefault(int(sg), c)
-        lasts[int(sg)] = c
-    segs = sorted(firsts)
-    order = []
-    lo, hi = 0, len(segs) - 1
-    while lo <= hi:
-        order.append(segs[lo])
-        if hi != lo:
-            order.append(segs[hi])
-        lo, hi = lo + 1, hi - 1
-    chosen, total = set(), 0
-    for sg in order:
-        for c in (firsts[sg], lasts[sg]):
-            if c in chosen:
-                continue
-            if chosen and total + int(lay.clen[c]) > budget_elems:
-                continue
-            chosen.add(c)
-            total += int(lay.clen[c])
-    if stride_chunks:
-        chosen.update(range(stride_chunks // 2, lay.nchunks, stride_chunks))
-    return np.array(sorted(chosen), dtype=np.int64)
+    first = np.ones(nch, bool)
+    first[1:] = seg[1:] != seg[:-1]
+    last = np.ones(nch, bool)
+    last[:-1] = seg[:-1] != seg[1:]
+    ragged = lay.clen != lay.clen.max()
+    must = first | last | ragged
+    rest = np.flatnonzero(~must)
+    n = int(lay.clen.sum())
+    s = max(1, int(stride))
+    while True:
+        pick = rest[s // 2::s]
+        chosen = np.union1d(np.flatnonzero(must), pick)
+        if s == 1 or int(lay.clen[chosen].sum()) >= min_frac * n:
+            return chosen.astype(np.int64)
+        s = max(1, (s * 4) // 5)
+
+
+def oracle_threads():
+    """Threads for the oracle side (ZO_ORACLE_THREADS, else at most 16 of the
+    cores this process may use)."""
+    env = os.environ.get("ZO_ORACLE_THREADS")
+    if env:
+        return max(1, int(env))
+    return max(1, min(16, len(os.sched_getaffinity(0))))
 
 
 # ---------------------------------------------------------------------------
 # oracle run (full shard or a sample of chunks)
 # ---------------------------------------------------------------------------
 
+def _runs(ids):
+    """Split sorted chunk ids into maximal runs of consecutive ids:
+    (first id, count) pairs."""
+    if len(ids) == 0:
+        return np.zeros(0, np.int64), np.zeros(0, np.int64)
+    brk = np.flatnonzero(np.diff(ids) != 1) + 1
+    starts = np.concatenate([[0], brk])
+    ends = np.concatenate([brk, [len(ids)]])
+    return ids[starts].astype(np.int64), (ends - starts).astype(np.int64)
+
+
 class OracleRun:
+    """The oracle on the chunks `chunk_ids` (sorted; default: every chunk) of a
+    workload, laid out back to back; inputs are generated at their global
+    indices."""
+
     def __init__(self, wl, chunk_ids=None, literal=False, grad_dtype="f32"):
         self.wl = wl
         self.grad_dtype = grad_dtype
@@ -87,10 +106,21 @@ class OracleRun:
         if chunk_ids is None:
             chunk_ids = np.arange(self.full.nchunks, dtype=np.int64)
         self.ids = np.asarray(chunk_ids, dtype=np.int64)
+        assert np.all(np.diff(self.ids) > 0), "chunk ids must be sorted and distinct"
         self.lay = orc.Layout.from_lengths(self.full.clen[self.ids])
-        self.ranges = [(int(self.full.cstart[c]), int(self.full.clen[c])) for c in self.ids]
-        self.wranges = [(int(self.full.cword[c]), int((self.full.clen[c] + 63) // 64))
-                        for c in self.ids]
+        self.n = self.lay.n
+        f = self.full
+        self.ranges = [(int(f.cstart[c]), int(f.clen[c])) for c in self.ids]
+        self.wranges = [(int(f.cword[c]), int((f.clen[c] + 63) // 64)) for c in self.ids]
+        # maximal runs of consecutive chunks: element, word and chunk ranges
+        c0, cnt = _runs(self.ids)
+        cl = c0 + cnt - 1
+        self.run_c0, self.run_nc = c0, cnt
+        self.run_e0 = f.cstart[c0] if len(c0) else np.zeros(0, np.int64)
+        self.run_ne = (f.cstart[cl] + f.clen[cl] - self.run_e0) if len(c0) else self.run_e0
+        self.run_w0 = f.cword[c0] if len(c0) else np.zeros(0, np.int64)
+        self.run_nw = (f.cword[cl] + (f.clen[cl] + 63) // 64 - self.run_w0) if len(c0) \
+            else self.run_w0
         x0 = self.gather_normal(C.STREAM_X, 0, wl.sigma_x)
         if wl.algorithm == "frozen-variance":
             self.worker = orc.FVWorker(self.lay, x0, wl.beta1, wl.beta2, wl.eps)
@@ -100,13 +130,8 @@ class OracleRun:
 
     def gather_normal(self, stream, step, sigma, per_mille=0, factor=1.0):
         k = synth.key(0, stream, step)
-        ks = C.ksigma(sigma)
-        if len(self.ranges) == 1 or self.lay.n == self.full.n:
-            return synth.normal_host(self.full.n, 0, k, ks, per_mille, factor) \
-                if self.lay.n == self.full.n else \
-                synth.normal_host(self.ranges[0][1], self.ranges[0][0], k, ks, per_mille, factor)
-        return np.concatenate([synth.normal_host(l, s, k, ks, per_mille, factor)
-                               for s, l in self.ranges])
+        return synth.normal_host_ranges(self.run_e0, self.run_ne, k, C.ksigma(sigma),
+                                        per_mille, factor)
 
     def grad(self, t):
         wl = self.wl
@@ -122,20 +147,17 @@ class OracleRun:
         wl = self.wl
         W = wl.world
         base = wl.peer_scale_base(t)
-        words = np.zeros((W - 1, self.lay.nwords), np.uint64)
-        scales = np.zeros((W - 1, self.lay.nchunks), np.float32)
+        words = np.empty((W - 1, self.lay.nwords), np.uint64)
+        scales = np.empty((W - 1, self.lay.nchunks), np.float32)
         for w in range(1, W):
-            kb = synth.key(w, C.STREAM_BITS, t)
-            ks = synth.key(w, C.STREAM_SCALES, t)
-            if self.lay.n == self.full.n:
-                words[w - 1] = synth.bits_host(self.full.nwords, 0, kb)
-                scales[w - 1] = synth.scales_host(self.full.nchunks, 0, ks, base)
-            else:
-                words[w - 1] = np.concatenate([synth.bits_host(nw, w0, kb)
-                                               for w0, nw in self.wranges])
-                scales[w - 1] = np.concatenate([synth.scales_host(1, int(c), ks, base)
-                                                for c in self.ids])
+            words[w - 1] = synth.bits_host_ranges(self.run_w0, self.run_nw,
+                                                  synth.key(w, C.STREAM_BITS, t))
+            scales[w - 1] = synth.scales_host_ranges(self.run_c0, self.run_nc,
+                                                     synth.key(w, C.STREAM_SCALES, t), base)
         return words, scales
+
+    def state(self, k):
+        return getattr(self.worker, k)
 
     def step(self, t):
         sync, var = steps_kind(self.wl, t)
@@ -149,6 +171,49 @@ class OracleRun:
                                     peer_scales=ps)
         return self.worker.step(self.wl.gamma(t), g, sync, var, gbar=gb, peer_words=pw,
                                 peer_scales=ps)
+
+
+class ParallelOracle:
+    """The oracle on a set of chunks, split into `parts` contiguous pieces of
+    about equal element counts, each an OracleRun stepped on its own thread
+    (the oracle and the input fills are C called through ctypes, which drops
+    the GIL).  Every computation of the method is local to a chunk, so the
+    pieces together compute exactly what one run over all the chunks would;
+    states and outputs are the pieces' in chunk order."""
+
+    OUT_KEYS = ("own_words", "own_scales", "srv_words", "srv_scales")
+
+    def __init__(self, wl, chunk_ids=None, parts=None, grad_dtype="f32"):
+        from concurrent.futures import ThreadPoolExecutor
+        self.wl = wl
+        self.full = orc.Layout.from_segments(wl.seg_off, wl.chunk)
+        if chunk_ids is None:
+            chunk_ids = np.arange(self.full.nchunks, dtype=np.int64)
+        ids = np.unique(np.asarray(chunk_ids, dtype=np.int64))
+        parts = max(1, min(parts or oracle_threads(), len(ids)))
+        cum = np.cumsum(self.full.clen[ids]) if len(ids) else np.zeros(0, np.int64)
+        tot = int(cum[-1]) if len(ids) else 0
+        cuts = [0] + [int(np.searchsorted(cum, tot * k / parts)) for k in range(1, parts)] + \
+            [len(ids)]
+        pieces = [ids[a:b] for a, b in zip(cuts[:-1], cuts[1:]) if b > a] or [ids]
+        self.runs = [OracleRun(wl, p, grad_dtype=grad_dtype) for p in pieces]
+        self.ids = ids
+        self.n = sum(r.n for r in self.runs)
+        self.ranges = [rg for r in self.runs for rg in r.ranges]
+        self.wranges = [rg for r in self.runs for rg in r.wranges]
+        self.pool = ThreadPoolExecutor(max_workers=len(self.runs))
+
+    def step(self, t):
+        outs = list(self.pool.map(lambda r: r.step(t), self.runs))
+        if not outs[0]:
+            return outs[0]
+        return {k: np.concatenate([o[k] for o in outs]) for k in self.OUT_KEYS}
+
+    def state(self, k):
+        return np.concatenate([r.state(k) for r in self.runs])
+
+    def close(self):
+        self.pool.shutdown()
 
 
 # ---------------------------------------------------------------------------
@@ -260,17 +325,24 @@ def gather_index(orun):
     return el, wd
 
 
+def _mismatches(gpu, ref):
+    """Elements that differ (binary32: -0 == +0; integers: exact)."""
+    return int(np.count_nonzero(~(gpu == ref)))
+
+
 class Comparator:
     def __init__(self, grun, orun):
         import torch
+        from concurrent.futures import ThreadPoolExecutor
         self.torch = torch
         self.grun, self.orun = grun, orun
         el, wd = gather_index(orun)
-        self.full = orun.lay.n == orun.full.n
+        self.full = orun.n == orun.full.n
         dev = grun.g.device
         self.el = torch.as_tensor(el, device=dev)
         self.wd = torch.as_tensor(wd, device=dev)
         self.ch = torch.as_tensor(orun.ids, device=dev)
+        self.pool = ThreadPoolExecutor(max_workers=4)
 
     def fetch(self, t, kind="elem"):
         if self.full:
@@ -282,33 +354,24 @@ class Comparator:
 
     def check(self, t, out):
         """Compare every state after step t; returns a dict of mismatch counts
-        (floats: -0 == +0; packed words: exact)."""
-        bad = {}
-        w = self.orun.worker
+        (floats: -0 == +0; packed words: exact).  The server range is the
+        whole shard, so the server error has the elements' indices."""
         self.torch.cuda.synchronize()
+        pairs = {}
         for k in self.grun.keys:
-            gpu = self.fetch(self.grun.opt.current(k))
-            ref = getattr(w, k)
-            if k == "srv_err" and not self.full:
-                pass  # the server range is the whole shard: same indices as elements
-            nbad = int(np.count_nonzero(~(gpu == ref)))
-            if nbad:
-                bad[k] = nbad
+            pairs[k] = (self.fetch(self.grun.opt.current(k)), self.orun.state(k))
         if out:
-            pw = self.fetch(self.grun.packed[0], "word").view(np.uint64)
-            if not np.array_equal(pw, out["own_words"]):
-                bad["own_words"] = int(np.count_nonzero(pw != out["own_words"]))
-            ps = self.fetch(self.grun.scales[0], "chunk")
-            if not np.array_equal(ps, out["own_scales"]):
-                bad["own_scales"] = int(np.count_nonzero(ps != out["own_scales"]))
-            sw = self.fetch(self.grun.srv_packed, "word").view(np.uint64)
-            ref_sw = out["srv_words"]
-            if not np.array_equal(sw, ref_sw):
-                bad["srv_words"] = int(np.count_nonzero(sw != ref_sw))
-            ss = self.fetch(self.grun.srv_scales, "chunk")
-            if not np.array_equal(ss, out["srv_scales"]):
-                bad["srv_scales"] = int(np.count_nonzero(ss != out["srv_scales"]))
-        return bad
+            pairs["own_words"] = (self.fetch(self.grun.packed[0], "word").view(np.uint64),
+                                  out["own_words"])
+            pairs["own_scales"] = (self.fetch(self.grun.scales[0], "chunk"), out["own_scales"])
+            pairs["srv_words"] = (self.fetch(self.grun.srv_packed, "word").view(np.uint64),
+                                  out["srv_words"])
+            pairs["srv_scales"] = (self.fetch(self.grun.srv_scales, "chunk"), out["srv_scales"])
+        counts = dict(zip(pairs, self.pool.map(lambda kv: _mismatches(*kv), pairs.values())))
+        return {k: v for k, v in counts.items() if v}
+
+    def close(self):
+        self.pool.shutdown()
 
 
 def run_parity(wl, steps=None, chunk_ids=None, fused=True, log=None, defer=False,
@@ -318,8 +381,14 @@ def run_parity(wl, steps=None, chunk_ids=None, fused=True, log=None, defer=False
     materialize_at: steps after which the deferred writes are forced out;
     grad_dtype: element type of the gradients handed to the library."""
     grun = GpuRun(wl, fused=fused, defer=defer, grad_dtype=grad_dtype)
-    orun = OracleRun(wl, chunk_ids, grad_dtype=grad_dtype)
+    orun = ParallelOracle(wl, chunk_ids, grad_dtype=grad_dtype)
     cmp_ = Comparator(grun, orun)
+    if log:
+        log(f"{wl.name}: oracle on {len(orun.ids)} of {orun.full.nchunks} chunks "
+            f"({orun.n} of {orun.full.n} elements, "
+            f"{int((orun.full.clen[orun.ids] != wl.chunk).sum())} of "
+            f"{int((orun.full.clen != wl.chunk).sum())} ragged chunks), "
+            f"{len(orun.runs)} threads")
     report = []
     try:
         bad = cmp_.check(-1, None)
@@ -338,5 +407,7 @@ def run_parity(wl, steps=None, chunk_ids=None, fused=True, log=None, defer=False
                 break
         inexact = grun.opt.inexact_chunks()
     finally:
+        cmp_.close()
+        orun.close()
         grun.close()
     return report, inexact

@@ -100,3 +100,33 @@ def test_traffic_summary_only_for_its_workload_and_source(tmp_path, monkeypatch)
                              "workload": "gpt2-1.5b",
                              "kernels": {"local+var": {"traffic_bytes": 1.0}}}))
     assert bench.measured_traffic("local+var", "deferred", "gpt2-1.5b") is None
+
+
+def test_variant_byte_model():
+    """Bytes of the kernel variants of the schedule: the general forms are the
+    whole-state figures (local 32, local+var 40, compress 20 + words, eager
+    reconstruction 24 + words, 32 with the variance line)."""
+    d, nch, nw, W = 1 << 20, 256, (1 << 20) // 64, 64
+    cp = 8 * nw + 4 * nch
+    vb = lambda name, gb=4: bench.variant_bytes(name, d, nch, nw, W, gb)
+    assert vb("local") == 32 * d and vb("local+var") == 40 * d
+    assert vb("sync1") == 20 * d + cp and vb("recon") == 24 * d + cp
+    assert vb("recon+var") == 32 * d + cp
+    assert vb("local (u=0)") == 20 * d + cp and vb("local (u=gm)") == 28 * d
+    assert vb("sync1 (u=0)") == 12 * d + 2 * cp and vb("sync1 (u=gm)") == 16 * d + cp
+    assert vb("recon (deferred)+var") == 20 * d + 2 * cp
+    assert vb("local", 2) == 30 * d and vb("local+var", 2) == 36 * d
+    for name in bench.VARIANT_KERNELS:
+        assert vb(name) > 0
+
+
+def test_kernel_names_map_to_variants():
+    """Template names from a kernel trace map back to the byte model's variants."""
+    for name, tmpl in bench.VARIANT_KERNELS.items():
+        for var in ((False, True) if name != "srv" and not name.startswith("sync1") else (False,)):
+            for gt, gb in ((0, 4), (2, 2)):
+                k = "zo::" + tmpl.format(var="true" if var else "false", gt=gt)
+                k = k.replace("L, V", "1024, 4").replace("LD, G", "512, 16")
+                assert bench.variant_of_kernel(k) == (name + ("+var" if var else ""),
+                                                      4 if name == "srv" else gb), k
+    assert bench.variant_of_kernel("zo::k_copy<true>") is None

@@ -117,7 +117,7 @@ def test_shard_beyond_2_31_elements(torch_cuda):
                     gammas=[1e-4] * T, sigma_g=1e-3)
     assert wl.n > 2 ** 31
     lay = orc.Layout.from_segments(wl.seg_off, wl.chunk)
-    ids = set(harness.sample_chunks(lay, wl.seg_off, 100000, 20000).tolist())
+    ids = set(harness.sample_chunks(lay, wl.seg_off).tolist())
     b = int(np.searchsorted(lay.cstart, 2 ** 31, side="right")) - 1  # holds element 2^31
     ids.update(range(b - 2, min(b + 3, lay.nchunks)))
     ids.add(lay.nchunks - 1)
@@ -181,6 +181,7 @@ def test_zero_gradient_segments(torch_cuda, defer):
                 assert not orun.worker.err[zero[0]:zero[1]].any()
         assert grun.opt.inexact_chunks() == 0
     finally:
+        cmp_.close()
         grun.close()
 
 
@@ -273,13 +274,19 @@ def test_pad_bits_of_inputs_are_ignored(torch_cuda):
 def test_inexact_scales_are_counted(torch_cuda):
     import harness
     torch = torch_cuda
-    wl = _wl(segs=(4096,), chunk=1024, world=4, T=1, tu=(0,), tv=())
+    wl = _wl(segs=(4096,), chunk=1024, world=4, T=2, tu=(0, 1), tv=())
     run = harness.GpuRun(wl)
     try:
         run.fill_inputs(0)
         run.opt.compress_pack_ef(0, wl.gamma(0), run.g, run.packed[0], run.scales[0])
         run.scales[1, 2] = 1.0e6        # 2^19 next to scales ~1e-8: span > 53 bits
         run.opt.unpack_average(0, run.packed, run.scales, run.srv_packed, run.srv_scales)
+        assert run.opt.inexact_chunks() == 1
+        # the flag stays set through later syncs whose scales are fine
+        run.opt.sync_update(0, run.srv_packed, run.srv_scales, None)
+        run.fill_inputs(1)
+        run.opt.compress_pack_ef(1, wl.gamma(1), run.g, run.packed[0], run.scales[0])
+        run.opt.unpack_average(1, run.packed, run.scales, run.srv_packed, run.srv_scales)
         assert run.opt.inexact_chunks() == 1
         torch.cuda.synchronize()
     finally:

@@ -81,7 +81,7 @@ def test_gpt2_sampled_bf16(torch_cuda):
     wl = dataclasses.replace(C.get("gpt2-1.5b"), name="gpt2-1.5b-alternating", steps=T,
                              tu=list(range(1, T, 2)), tv=list(range(T)), gammas=[1e-4] * T)
     lay = orc.Layout.from_segments(wl.seg_off, wl.chunk)
-    ids = harness.sample_chunks(lay, wl.seg_off, 150000, 30000)
+    ids = harness.sample_chunks(lay, wl.seg_off)
     report, inexact = harness.run_parity(wl, chunk_ids=ids, log=_log, defer=True,
                                          grad_dtype="bf16")
     _assert_clean(report, inexact)

@@ -40,6 +40,10 @@ MUTANTS = [
     ("fv-new-momentum", "        float step = gamma * m_old;\n        float den = sqrtf(v_old + p->eps);\n        x[j]",
      "        float step = gamma * m[j];\n        float den = sqrtf(v_old + p->eps);\n        x[j]"),
     ("fv-variance-always", "        if (update_v) v[j] =", "        v[j] ="),
+    ("dense-average-worker-index", "            double term = (double)z[(int64_t)w * n + j];",
+     "            double term = (double)z[(int64_t)j * W + w];"),
+    ("dense-average-first-worker-only", "            double term = (double)z[(int64_t)w * n + j];",
+     "            double term = (double)z[j];"),
 ]
 
 

@@ -288,6 +288,55 @@ def test_server_single_worker_and_equal_signs():
     np.testing.assert_array_equal(avg, np.where(bits == 1, mag, -mag).astype(F32))
 
 
+@pytest.mark.parametrize("W", [2, 3, 5, 7, 16])
+def test_dense_average_is_exact_rounding(W):
+    """The compression-off average of W dense buffers (worker-major [W][n]):
+    the exact rational mean of the W values at each position, rounded once to
+    binary32.  Worker values differ in sign, magnitude and position, so a
+    wrong worker or element index changes the result."""
+    n = 300
+    r = rng(2000 + W)
+    z = (r.standard_normal((W, n)) * r.choice([1e-8, 3e-7, 2e-6], size=(W, 1))).astype(F32)
+    got = orc.dense_average(z)
+    for j in range(n):
+        want = rn32(sum(Fraction(float(z[w, j])) for w in range(W)) / W)
+        assert got[j] == want, (j, W)
+    # the same buffers in another worker order average to the same values
+    np.testing.assert_array_equal(orc.dense_average(z[::-1].copy()), got)
+    # one worker: the buffer itself
+    np.testing.assert_array_equal(orc.dense_average(z[:1].copy()), z[0])
+
+
+def test_dense_average_flags_inexact_sum():
+    z = np.array([[1.0, 1.0], [2.0 ** -60, 0.0]], F32)
+    with pytest.raises(orc.OracleError):
+        orc.dense_average(z)
+
+
+@pytest.mark.parametrize("W", [3, 5, 6, 7, 9, 11, 100, 127, 65535])
+def test_binary64_quotient_by_w_rounds_once(W):
+    """Both sides form the average as (float)(S / W) from the exact binary64
+    sum S: two roundings.  For a binary64 S and an integer W the result is
+    still RN32(S / W) -- if RN64(S / W) landed on a binary32 midpoint M while
+    S / W != M, then |S - W M| >= ulp64(S) and |S / W - M| < ulp64(M) / 2
+    would force 2^(e(S) - e(M) + 1) < W, while e(S) >= e(M) + floor(log2 W)
+    -- checked here on sums right next to W times binary32 midpoints, where a
+    double rounding would show."""
+    r = rng(3000 + W)
+    for _ in range(400):
+        f = F32(r.uniform(0.5, 1.0) * 2.0 ** int(r.integers(-40, 40)))
+        if r.random() < 0.5:
+            f = -f
+        mid = (Fraction(float(f)) + Fraction(float(np.nextafter(f, F32(np.inf))))) / 2
+        s0 = float(mid * W)
+        for k in range(-3, 4):
+            s = s0
+            for _ in range(abs(k)):
+                s = float(np.nextafter(s, np.inf if k > 0 else -np.inf))
+            got = F32(np.float64(s) / np.float64(W))
+            assert got == rn32(Fraction(s) / W), (W, float(f), k)
+
+
 def test_server_flags_inexact_sum():
     lay = orc.Layout.from_lengths([64])
     words_w = np.array([[0], [0xFFFFFFFFFFFFFFFF]], np.uint64)
