@@ -111,6 +111,30 @@ def summarize_counters(dirs, mode):
         print(f"| {label} | " + " | ".join(ratio(k, a, b) for k in names) + " |")
 
 
+def trace_rows(trace_dir):
+    """Kernel dispatches of a rocprofv3 --kernel-trace run under `trace_dir`,
+    from its CSV files or its SQLite results database (the `kernels` view), as
+    dicts with Kernel_Name, Start_Timestamp, End_Timestamp (ns) and
+    Grid_Size_X."""
+    rows = []
+    for root, _, files in os.walk(trace_dir):
+        for fn in sorted(files):
+            path = os.path.join(root, fn)
+            if fn.endswith("kernel_trace.csv"):
+                rows += list(csv.DictReader(open(path)))
+            elif fn.endswith("_results.db"):
+                import sqlite3
+                con = sqlite3.connect(path)
+                try:
+                    for name, start, end, grid in con.execute(
+                            "select name, start, end, grid_x from kernels"):
+                        rows.append({"Kernel_Name": name, "Start_Timestamp": start,
+                                     "End_Timestamp": end, "Grid_Size_X": grid})
+                finally:
+                    con.close()
+    return rows
+
+
 def summarize_trace(trace_dir, mode, workload, warmup, steps):
     """Per-kernel durations of a `rocprofv3 --kernel-trace` run of this bench
     (the default command: `warmup` + `steps` bench steps) over the timed
@@ -128,11 +152,7 @@ def summarize_trace(trace_dir, mode, workload, warmup, steps):
               ("srv", r"zo::k_srv_(lut|plain)<"), ("fv_apply", r"zo::k_fv_apply")] if fv else
              [("local+var", r"zo::k_local<"), ("sync1", r"zo::k_sync1<"),
               ("srv", r"zo::k_srv_(lut|plain)<"), ("recon+var", r"zo::k_recon<")])
-    rows = []
-    for root, _, files in os.walk(trace_dir):
-        for fn in files:
-            if fn.endswith("kernel_trace.csv"):
-                rows += list(csv.DictReader(open(os.path.join(root, fn))))
+    rows = trace_rows(trace_dir)
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
     wl = C.get(workload)
     _, ln, _, nwords = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
@@ -183,11 +203,7 @@ def summarize_kernels(trace_dir, workload):
     import statistics
     import paper_2202_06009_amd as zo
     from synth import configs as C
-    rows = []
-    for root, _, files in os.walk(trace_dir):
-        for fn in files:
-            if fn.endswith("kernel_trace.csv"):
-                rows += list(csv.DictReader(open(os.path.join(root, fn))))
+    rows = trace_rows(trace_dir)
     wl = C.get(workload)
     _, ln, _, nwords = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
     groups = {}
