@@ -92,7 +92,10 @@ typedef struct zo_adam zo_adam;   /* opaque handle */
  *   beta1, beta2   Adam decay factors, each in [0, 1) (Algorithm 1 inputs).
  *   eps            numerical constant added inside the square root, >= 0.
  *   world          number of workers n = W >= 1 (the average of Algorithm 2).
- *   chunk          compression chunk length C: a multiple of 4 in [4, 16384].
+ *   chunk          compression chunk length C in [1, 16384].  Chunks then
+ *                  start at segment offsets plus multiples of C; when C is not a
+ *                  multiple of 4 the chunk kernels access elements one by one
+ *                  (slower) and the server uses its plain form.
  *   n              shard length d >= 0.
  *   nseg, seg_off  nseg >= 1 segments; seg_off[0] = 0, seg_off[nseg] = n,
  *                  non-decreasing, every offset a multiple of 4.

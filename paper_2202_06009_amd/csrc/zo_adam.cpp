@@ -43,7 +43,7 @@ bool strictly_increasing(const int64_t *v, int32_t n)
 int check_segments(int32_t nseg, const int64_t *seg_off, int32_t chunk)
 {
     if (nseg < 1 || !seg_off) return ZO_EINVAL;
-    if (chunk < 4 || chunk > kMaxChunk || chunk % 4) return ZO_EINVAL;
+    if (chunk < 1 || chunk > kMaxChunk) return ZO_EINVAL;
     if (seg_off[0] != 0) return ZO_EINVAL;
     for (int32_t s = 0; s < nseg; ++s)
         if (seg_off[s + 1] < seg_off[s]) return ZO_EINVAL;
@@ -57,6 +57,7 @@ int check_segments(int32_t nseg, const int64_t *seg_off, int32_t chunk)
 struct zo_adam {
     zo::Scalars sc{};
     int32_t world = 1, chunk = 4;
+    bool al = true;  // chunk % 4 == 0: every chunk starts and ends on a float4
     int64_t n = 0, nchunks = 0, nwords = 0;
     std::vector<int64_t> hstart, hword;
     std::vector<int32_t> hlen;
@@ -188,6 +189,7 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
     h->sc.c2 = 1.0f - cfg->beta2;
     h->world = cfg->world;
     h->chunk = cfg->chunk;
+    h->al = cfg->chunk % 4 == 0;
     h->n = cfg->n;
     h->geo = zo::geometry_for(cfg->chunk);
     h->st = *st;
@@ -330,7 +332,7 @@ int zo_local_step(zo_adam *h, int64_t t, float gamma, const void *g, const void 
     s.gamma_u = h->gamma_u;
     hipError_t e = zo::launch_local(gbar != nullptr, h->u_in, write_u, g, h->st.m, x_src,
                                     h->st.x, h->st.v, h->st.u, gbar, h->n, s, h->gt, h->ch,
-                                    h->nchunks, h->chunk, h->sm, h->stream);
+                                    h->nchunks, h->chunk, h->al, h->sm, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     h->x_in_anchor = false;
     if (write_u) {
@@ -364,7 +366,7 @@ int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const void *g, uint6
         zo::Scalars s = h->sc;
         hipError_t e = zo::launch_sync1(h->geo, false, zo::U_MEM, nullptr, nullptr, g, h->st.err,
                                         h->ch, h->nchunks, packed0, scales0, s, zo::GT_F32,
-                                        h->gt, h->sm, h->stream);
+                                        h->gt, h->al, h->sm, h->stream);
         if (e != hipSuccess) return h->hip_fail(e);
         h->fv_gamma = gamma;
         h->phase = PH_COMPRESSED;
@@ -385,7 +387,7 @@ int zo_compress_pack_ef(zo_adam *h, int64_t t, float gamma, const void *g, uint6
     // unfused path)
     hipError_t e = zo::launch_sync1(h->geo, fused, fused ? h->u_in : zo::U_MEM, g, h->st.m,
                                     h->st.u, h->st.err, h->ch, h->nchunks, packed0, scales0, s,
-                                    h->gt, zo::GT_F32, h->sm, h->stream);
+                                    h->gt, zo::GT_F32, h->al, h->sm, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     if (fused) h->gamma_sum = h->gamma_sum + gamma;
     h->phase = PH_COMPRESSED;
@@ -405,7 +407,7 @@ int zo_unpack_average(zo_adam *h, int64_t t, const uint64_t *packed, const float
     hipError_t e = zo::launch_srv(h->geo, h->srv_algo, packed, scales, h->world, h->w1 - h->w0,
                                   nch, h->ch, h->c0, nch, h->w0, h->e0, h->st.srv_err,
                                   srv_packed, srv_scales, avg_debug, h->dflags, h->chunk,
-                                  h->stream);
+                                  h->al, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     h->phase = PH_AVERAGED;
     return ZO_OK;
@@ -424,7 +426,7 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
         zo::Scalars s = h->sc;
         s.gamma = h->fv_gamma;
         hipError_t e = zo::launch_fv_apply(srv_packed, srv_scales, h->ch, h->nchunks, h->st.x,
-                                           h->st.m, h->st.v, s, h->chunk, h->stream);
+                                           h->st.m, h->st.v, s, h->chunk, h->al, h->stream);
         if (e != hipSuccess) return h->hip_fail(e);
         h->finish_step();
         return ZO_OK;
@@ -434,10 +436,10 @@ int zo_sync_update(zo_adam *h, int64_t t, const uint64_t *srv_packed, const floa
     // the deferred kernel reads the anchor, which holds x_{t'} in both cases
     zo::SrvCopy sm = h->sm;
     sm.gamma_m = h->gamma_sum;
-    hipError_t e = zo::launch_recon(h->geo, gbar != nullptr, h->defer, srv_packed, srv_scales,
-                                    h->ch, h->nchunks, h->st.m, h->st.x, h->st.v, h->st.u,
-                                    h->st.anchor, gbar, h->gamma_sum, h->sc, h->gt, h->chunk, sm,
-                                    h->stream);
+    hipError_t e = zo::launch_recon(gbar != nullptr, h->defer, srv_packed, srv_scales, h->ch,
+                                    h->nchunks, h->st.m, h->st.x, h->st.v, h->st.u,
+                                    h->st.anchor, gbar, h->gamma_sum, h->sc, h->gt, h->chunk,
+                                    h->al, sm, h->stream);
     if (e != hipSuccess) return h->hip_fail(e);
     if (h->defer) {
         h->x_in_anchor = true;
@@ -501,7 +503,8 @@ int zo_read_state(zo_adam *h, int32_t which, float *out)
         e = zo::launch_copy(h->x_in_anchor ? h->st.anchor : h->st.x, out, h->n, true, h->stream);
     } else if (which == ZO_STATE_M) {
         e = h->u_in == zo::U_ZERO
-                ? zo::launch_m_from_copy(out, h->ch, h->nchunks, h->chunk, h->sm, h->stream)
+                ? zo::launch_m_from_copy(out, h->ch, h->nchunks, h->chunk, h->al, h->sm,
+                                         h->stream)
                 : zo::launch_copy(h->st.m, out, h->n, true, h->stream);
     } else if (h->u_in == zo::U_ZERO) {
         e = zo::launch_zero(out, h->n, h->stream);
@@ -525,7 +528,8 @@ int zo_materialize(zo_adam *h)
     if (h->u_in == zo::U_ZERO) {
         hipError_t e = zo::launch_zero(h->st.u, h->n, h->stream);
         if (e == hipSuccess)
-            e = zo::launch_m_from_copy(h->st.m, h->ch, h->nchunks, h->chunk, h->sm, h->stream);
+            e = zo::launch_m_from_copy(h->st.m, h->ch, h->nchunks, h->chunk, h->al, h->sm,
+                                       h->stream);
         if (e != hipSuccess) return h->hip_fail(e);
     } else if (h->u_in == zo::U_GM) {
         hipError_t e = zo::launch_u_from_m(h->st.u, h->st.m, h->n, h->gamma_u, h->stream);
@@ -618,7 +622,8 @@ int zo_diag_server_pattern(zo_adam *h, const uint64_t *packed)
     const int64_t nch = h->c1 - h->c0;
     if (nch > 0 && !packed) return ZO_EINVAL;
     if (!aligned(packed, 8)) return ZO_EALIGN;
-    if (h->chunk <= 1024) return ZO_EINVAL;  // the server's one-chunk-per-workgroup shapes
+    // the server's one-chunk-per-workgroup shapes, aligned chunks only
+    if (h->chunk <= 1024 || !h->al) return ZO_EINVAL;
     hipError_t e = zo::launch_srv_pattern(h->chunk, packed, h->world, h->w1 - h->w0, h->ch, h->c0,
                                           nch, h->w0, h->e0, h->st.srv_err, h->stream);
     return e == hipSuccess ? ZO_OK : h->hip_fail(e);

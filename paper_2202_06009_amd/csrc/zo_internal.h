@@ -45,7 +45,7 @@ struct Chunks {
 
 // Mapping of one chunk onto a workgroup: L lanes per chunk (a power of two
 // <= 1024; several chunks share a 256-thread workgroup when L < 256), V blocks
-// of 4L elements per lane (a power of two, > 1 only when L = 1024).
+// of 4L elements per lane (1, 2 or 4; > 1 only when L = 1024).
 // 4 * L * V >= the configured chunk length.
 struct Geometry {
     int L, V;
@@ -59,15 +59,19 @@ enum GradType { GT_F32 = 0, GT_F16 = 1, GT_BF16 = 2 };
 // Server-average algorithm.
 enum SrvAlgo { SRV_AUTO = 0, SRV_PLAIN = 1 };
 
+// `al` (every launcher of a chunk kernel): every chunk length is a multiple of
+// 4, so every chunk starts and ends on a 16-byte boundary and its lanes use
+// float4 accesses; otherwise the unaligned forms (zo_kernels_ua.hip).
+
 // u_in: where u is (BufferIn; U_ZERO also takes m from `sm`, over the chunk
 // grid); write_u: false only with U_ZERO, leaving u = gamma * m implicit;
 // x_src may equal x.
 hipError_t launch_local(bool var, int u_in, bool write_u, const void *g, float *m,
                         const float *x_src, float *x, float *v, float *u, const void *gbar,
                         int64_t n, const Scalars &s, int gt, const Chunks &ch, int64_t nchunks,
-                        int chunk, const SrvCopy &sm, hipStream_t st);
+                        int chunk, bool al, const SrvCopy &sm, hipStream_t st);
 // m = (bit ? S_c : -S_c) / gamma_m from the server copy, over the shard.
-hipError_t launch_m_from_copy(float *m, const Chunks &ch, int64_t nchunks, int chunk,
+hipError_t launch_m_from_copy(float *m, const Chunks &ch, int64_t nchunks, int chunk, bool al,
                               const SrvCopy &sm, hipStream_t st);
 // u = +0 + gamma_u * m (writes out an implicit U_GM buffer).
 hipError_t launch_u_from_m(float *u, const float *m, int64_t n, float gamma_u, hipStream_t st);
@@ -80,26 +84,26 @@ hipError_t launch_var(float *v, const void *gbar, int64_t n, const Scalars &s, i
 hipError_t launch_sync1(Geometry geo, bool fused, int u_in, const void *g, const float *m,
                         const void *u, float *err, const Chunks &ch, int64_t nchunks,
                         uint64_t *packed, float *scales, const Scalars &s, int gt, int ut,
-                        const SrvCopy &sm, hipStream_t st);
+                        bool al, const SrvCopy &sm, hipStream_t st);
 hipError_t launch_srv(Geometry geo, int algo, const uint64_t *packed, const float *scales, int W,
                       int64_t wstride, int64_t cstride, const Chunks &ch, int64_t c0,
                       int64_t nch, int64_t word0, int64_t elem0, float *srv_err,
                       uint64_t *srv_packed, float *srv_scales, float *avg, uint8_t *flags,
-                      int chunk, hipStream_t st);
+                      int chunk, bool al, hipStream_t st);
 // defer: write the anchor and `sm` only (the model stays in the anchor, u = 0
 // and m = the server average / Gamma implicit).
-hipError_t launch_recon(Geometry geo, bool var, bool defer, const uint64_t *srv_packed,
+hipError_t launch_recon(bool var, bool defer, const uint64_t *srv_packed,
                         const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
                         float *x, float *v, float *u, float *anchor, const void *gbar,
-                        float gsum, const Scalars &s, int gt, int chunk, const SrvCopy &sm,
-                        hipStream_t st);
+                        float gsum, const Scalars &s, int gt, int chunk, bool al,
+                        const SrvCopy &sm, hipStream_t st);
 // Algorithm 4: the full-precision step (t in T_v) and the step from the
 // server's compressed average (t outside T_v).
 hipError_t launch_fv_full(const void *gbar, float *x, float *m, float *v, int64_t n,
                           const Scalars &s, int gt, hipStream_t st);
 hipError_t launch_fv_apply(const uint64_t *srv_packed, const float *srv_scales, const Chunks &ch,
                            int64_t nchunks, float *x, float *m, const float *v, const Scalars &s,
-                           int chunk, hipStream_t st);
+                           int chunk, bool al, hipStream_t st);
 hipError_t launch_copy(const float *src, float *dst, int64_t n, bool nt, hipStream_t st);
 
 // Streams of the HBM-mix diagnostic: up to 6 read and 4 write arrays.
@@ -113,5 +117,27 @@ hipError_t launch_srv_pattern(int chunk, const uint64_t *packed, int W, int64_t 
                               int64_t elem0, float *srv_err, hipStream_t st);
 hipError_t launch_divsqrt(const float *a, const float *b, float *q, float *r, int64_t n,
                           hipStream_t st);
+
+// The unaligned forms of the chunk launchers (zo_kernels_ua.hip), called by
+// the launchers above when `al` is false.
+hipError_t launch_local_zero_ua(bool var, bool write_u, const void *g, float *m,
+                                const float *x_src, float *x, float *v, float *u,
+                                const void *gbar, int64_t n4, const Scalars &s, int gt,
+                                const Chunks &ch, int64_t nchunks, int chunk, const SrvCopy &sm,
+                                hipStream_t st);
+hipError_t launch_m_from_copy_ua(float *m, const Chunks &ch, int64_t nchunks, int chunk,
+                                 const SrvCopy &sm, hipStream_t st);
+hipError_t launch_sync1_ua(Geometry geo, bool fused, int u_in, const void *g, const float *m,
+                           const void *u, float *err, const Chunks &ch, int64_t nchunks,
+                           uint64_t *packed, float *scales, const Scalars &s, int gt, int ut,
+                           const SrvCopy &sm, hipStream_t st);
+hipError_t launch_fv_apply_ua(const uint64_t *srv_packed, const float *srv_scales,
+                              const Chunks &ch, int64_t nchunks, float *x, float *m,
+                              const float *v, const Scalars &s, int chunk, hipStream_t st);
+hipError_t launch_recon_ua(bool var, bool defer, const uint64_t *srv_packed,
+                           const float *srv_scales, const Chunks &ch, int64_t nchunks, float *m,
+                           float *x, float *v, float *u, float *anchor, const void *gbar,
+                           float gsum, const Scalars &s, int gt, int chunk, const SrvCopy &sm,
+                           hipStream_t st);
 
 }  // namespace zo

@@ -57,7 +57,10 @@ def _cfg(**over):
     ({"eps": float("inf")}, zo.ZO_EINVAL),
     ({"world": 0}, zo.ZO_EINVAL),
     ({"chunk": 0}, zo.ZO_EINVAL),
-    ({"chunk": 6}, zo.ZO_EINVAL),
+    ({"chunk": 1}, zo.ZO_OK),
+    ({"chunk": 6}, zo.ZO_OK),
+    ({"chunk": 16383}, zo.ZO_OK),
+    ({"chunk": 16385}, zo.ZO_EINVAL),
     ({"chunk": 16388}, zo.ZO_EINVAL),
     ({"chunk": 16384}, zo.ZO_OK),
     ({"chunk": 4}, zo.ZO_OK),
@@ -94,10 +97,10 @@ def test_chunk_plan_matches_oracle_layout(name):
 
 @settings(max_examples=200, deadline=None)
 @given(lens=st.lists(st.integers(0, 3000).map(lambda v: 4 * v), min_size=1, max_size=12),
-       chunk=st.integers(1, 4096).map(lambda v: 4 * v))
+       chunk=st.integers(1, 16384))
 def test_chunk_plan_properties(lens, chunk):
-    """Random segment tables (empty segments, ragged tails, any chunk that is a
-    multiple of 4 up to 16384): the library's plan equals the oracle's, its
+    """Random segment tables (empty segments, ragged tails, any chunk
+    length from 1 to 16384): the library's plan equals the oracle's, its
     chunks tile every segment in order without crossing a boundary, and each
     chunk's packed words start where the previous chunk's 64-element words end."""
     import oracle as orc
