@@ -71,7 +71,8 @@ enum {
     ZO_EALIGN = -2,   /* pointer not 16-byte aligned / segment offset not a multiple of 4 */
     ZO_ESTATE = -3,   /* call out of order for the current step */
     ZO_EHIP = -4,     /* HIP runtime error (text via zo_last_hip_error) */
-    ZO_ENOMEM = -5    /* host or device allocation failed in zo_adam_init */
+    ZO_ENOMEM = -5,   /* host or device allocation failed in zo_adam_init */
+    ZO_ESCRATCH = -6  /* zo_adam_init_static: the configuration exceeds its static scratch */
 };
 
 /* Element types of the gradient inputs (zo_config.grad_dtype). */
@@ -176,6 +177,27 @@ typedef struct zo_state {
  * Returns ZO_OK and *h, or an error (then *h is NULL).
  */
 int zo_adam_init(zo_adam **h, const zo_config *cfg, const zo_state *st, hipStream_t stream);
+
+/*
+ * zo_adam_init_static -- zo_adam_init for callers that cannot allocate
+ * (code recorded under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): the same handle, arguments, validation, initial state
+ * and results, but no device or host memory is allocated.  The chunk table,
+ * the exactness flags and, with defer_sync_writes, the copy of the server's
+ * output live in the library's static device array of 4 MiB (each GPU the
+ * library runs on holds one until the process ends), the handle and its
+ * schedules in a static host slot of the current device.
+ * Limits: one live handle from zo_adam_init_static per device at a time
+ * (ZO_ESTATE while one exists; zo_adam_destroy frees the slot; a later one
+ * reuses the array and starts from a cleared state); 20 bytes per chunk plus
+ * one per server chunk, plus 8 per packed word and 4 per chunk with
+ * defer_sync_writes, must fit the 4 MiB (about 190,000 chunks without
+ * deferred writes), and T_v and T_u at most 65536 steps each, else
+ * ZO_ESCRATCH.  Calls on such a handle from several host threads race, as on
+ * any handle.  zo_chunk_table reads the table back from the device.
+ */
+int zo_adam_init_static(zo_adam **h, const zo_config *cfg, const zo_state *st,
+                        hipStream_t stream);
 
 /* Release the handle and its device memory.  Waits for the stream. */
 int zo_adam_destroy(zo_adam *h);

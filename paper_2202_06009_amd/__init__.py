@@ -13,7 +13,7 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libzoadam.so")
 
-ZO_OK, ZO_EINVAL, ZO_EALIGN, ZO_ESTATE, ZO_EHIP, ZO_ENOMEM = 0, -1, -2, -3, -4, -5
+ZO_OK, ZO_EINVAL, ZO_EALIGN, ZO_ESTATE, ZO_EHIP, ZO_ENOMEM, ZO_ESCRATCH = 0, -1, -2, -3, -4, -5, -6
 ZO_ALG_ZERO_ONE_ADAM, ZO_ALG_FROZEN_VARIANCE = 0, 1
 ZO_DTYPE_F32, ZO_DTYPE_F16, ZO_DTYPE_BF16 = 0, 1, 2
 GRAD_DTYPES = {"f32": ZO_DTYPE_F32, "f16": ZO_DTYPE_F16, "bf16": ZO_DTYPE_BF16}
@@ -21,7 +21,7 @@ ALGORITHMS = {"zero-one": ZO_ALG_ZERO_ONE_ADAM, "frozen-variance": ZO_ALG_FROZEN
 
 # Every function the header declares (checked by the CPU export test).
 EXPORTS = (
-    "zo_adam_init", "zo_adam_destroy", "zo_set_stream", "zo_local_step",
+    "zo_adam_init", "zo_adam_init_static", "zo_adam_destroy", "zo_set_stream", "zo_local_step",
     "zo_compress_pack_ef", "zo_unpack_average", "zo_sync_update", "zo_variance_update",
     "zo_fullprec_step", "zo_materialize", "zo_state_location", "zo_read_state", "zo_num_chunks",
     "zo_packed_words",
@@ -72,6 +72,8 @@ def lib():
         sig = {
             "zo_adam_init": ([ctypes.POINTER(vp), ctypes.POINTER(_Config),
                               ctypes.POINTER(_State), vp], ci),
+            "zo_adam_init_static": ([ctypes.POINTER(vp), ctypes.POINTER(_Config),
+                                     ctypes.POINTER(_State), vp], ci),
             "zo_adam_destroy": ([vp], ci),
             "zo_set_stream": ([vp, vp], ci),
             "zo_local_step": ([vp, i64, f32, vp, vp], ci),
@@ -182,16 +184,19 @@ def zo_plan_chunks(seg_off, chunk):
     return list(st)[:nch], list(ln)[:nch], list(wd)[:nch], nw
 
 
-def zo_adam_init(cfg_kwargs, state, stream=None):
+def zo_adam_init(cfg_kwargs, state, stream=None, static=False):
+    """zo_adam_init, or zo_adam_init_static (no allocation) with static=True."""
     cfg, keep = make_config(**cfg_kwargs)
     keys = ("x", "m", "v", "u", "err", "srv_err", "anchor")
     st = _State(**{k: (state[k].data_ptr() if state.get(k) is not None else None) for k in keys})
     for k in keys:
         _ptr(state.get(k))
     h = ctypes.c_void_p()
-    rc = lib().zo_adam_init(ctypes.byref(h), ctypes.byref(cfg), ctypes.byref(st), _stream(stream))
+    name = "zo_adam_init_static" if static else "zo_adam_init"
+    rc = getattr(lib(), name)(ctypes.byref(h), ctypes.byref(cfg), ctypes.byref(st),
+                              _stream(stream))
     if rc != ZO_OK:
-        raise ZoError(rc, "zo_adam_init")
+        raise ZoError(rc, name)
     return h
 
 
@@ -313,7 +318,7 @@ class ZoAdam:
 
     def __init__(self, *, beta1, beta2, eps, world, chunk, seg_off, tv=(), tu=(), state,
                  srv_chunk_begin=0, srv_chunk_end=-1, defer_sync_writes=False,
-                 algorithm="zero-one", grad_dtype="f32", stream=None):
+                 algorithm="zero-one", grad_dtype="f32", stream=None, static=False):
         self.cfg = dict(beta1=beta1, beta2=beta2, eps=eps, world=world, chunk=chunk,
                         seg_off=list(seg_off), tv=list(tv), tu=list(tu),
                         srv_chunk_begin=srv_chunk_begin, srv_chunk_end=srv_chunk_end,
@@ -331,7 +336,7 @@ class ZoAdam:
         if self.r_elems:
             _need(state.get("srv_err"), "state['srv_err']", "float32", self.r_elems)
         self.state = state
-        self.h = zo_adam_init(self.cfg, state, stream)
+        self.h = zo_adam_init(self.cfg, state, stream, static=static)
 
     def _sizes(self):
         """Shard length, chunks, packed words and the server range, from the

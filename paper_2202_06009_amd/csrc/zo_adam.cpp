@@ -10,6 +10,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -91,8 +92,16 @@ struct zo_adam {
     uintptr_t galign = 16;        // their alignment: one float4 of elements
     char hip_err[192] = {0};
 
-    bool in_tv(int64_t s) const { return std::binary_search(tv.begin(), tv.end(), s); }
-    bool in_tu(int64_t s) const { return std::binary_search(tu.begin(), tu.end(), s); }
+    // the schedules T_v and T_u: the vectors above, or a static slot's arrays
+    const int64_t *tvp = nullptr, *tup = nullptr;
+    int64_t ntv = 0, ntu = 0;
+    // zo_adam_init_static: the device whose static slot holds this handle
+    // (its chunk table, flags and server copy are in that device's scratch
+    // array; no host chunk table is kept); -1 for zo_adam_init
+    int slot = -1;
+
+    bool in_tv(int64_t s) const { return std::binary_search(tvp, tvp + ntv, s); }
+    bool in_tu(int64_t s) const { return std::binary_search(tup, tup + ntu, s); }
 
     int hip_fail(hipError_t e)
     {
@@ -165,23 +174,29 @@ int zo_config_check(const zo_config *cfg)
     return ZO_OK;
 }
 
-int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStream_t stream)
+}  // extern "C"
+
+namespace {
+
+// The state pointers zo_adam_init requires (Algorithm 4 has no buffer u and
+// no anchor), each 16-byte aligned.
+int check_state(const zo_config *cfg, const zo_state *st)
 {
-    if (!out) return ZO_EINVAL;
-    *out = nullptr;
-    int rc = zo_config_check(cfg);
-    if (rc) return rc;
     if (!st) return ZO_EINVAL;
     const bool fv = cfg->algorithm == ZO_ALG_FROZEN_VARIANCE;
     const float *ptrs[] = {st->x, st->m, st->v, st->err, st->srv_err, st->u, st->anchor};
     for (int i = 0; i < 7; ++i) {
-        const bool needed = i < 5 || !fv;  // Algorithm 4 has no buffer u and no anchor
+        const bool needed = i < 5 || !fv;
         if (cfg->n > 0 && needed && !ptrs[i]) return ZO_EINVAL;
         if (!aligned(ptrs[i], 16)) return ZO_EALIGN;
     }
+    return ZO_OK;
+}
 
-    zo_adam *h = new (std::nothrow) zo_adam();
-    if (!h) return ZO_ENOMEM;
+// Every field of a handle that comes from the configuration, except the
+// schedules and the chunk table (no allocation).
+void set_fields(zo_adam *h, const zo_config *cfg, const zo_state *st, hipStream_t stream)
+{
     h->sc.b1 = cfg->beta1;
     h->sc.b2 = cfg->beta2;
     h->sc.eps = cfg->eps;
@@ -194,17 +209,160 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
     h->geo = zo::geometry_for(cfg->chunk);
     h->st = *st;
     h->stream = stream;
-    h->tv.assign(cfg->tv, cfg->tv + cfg->ntv);
-    h->tu.assign(cfg->tu, cfg->tu + cfg->ntu);
     h->defer = cfg->defer_sync_writes != 0;
-    h->fv = fv;
+    h->fv = cfg->algorithm == ZO_ALG_FROZEN_VARIANCE;
     h->gt = cfg->grad_dtype == ZO_DTYPE_F16 ? zo::GT_F16
             : cfg->grad_dtype == ZO_DTYPE_BF16 ? zo::GT_BF16 : zo::GT_F32;
     h->galign = h->gt == zo::GT_F32 ? 16 : 8;
-
     h->nchunks = zo_plan_num_chunks(cfg->nseg, cfg->seg_off, cfg->chunk);
+    h->c0 = cfg->srv_chunk_begin;
+    h->c1 = cfg->srv_chunk_end < 0 ? h->nchunks : cfg->srv_chunk_end;
+}
+
+// Bytes of the device block a handle uses: the chunk table (start, word,
+// length), one exactness flag per server chunk and, with deferred sync
+// writes, the copy of the server's packed words and scales at copy_off.
+size_t device_block(const zo_adam *h, size_t &copy_off)
+{
+    const size_t nb = (size_t)h->nchunks;
+    copy_off = (nb * (8 + 8 + 4) + (size_t)(h->c1 - h->c0) + 64 + 255) & ~(size_t)255;
+    const size_t copy_bytes = h->defer ? (size_t)h->nwords * 8 + nb * 4 : 0;
+    return nb ? copy_off + copy_bytes : 0;
+}
+
+// Point the handle's device views into the block at `base`.
+void place_block(zo_adam *h, char *base, size_t copy_off)
+{
+    const size_t nb = (size_t)h->nchunks;
+    h->ch.start = (const int64_t *)base;
+    h->ch.word = (const int64_t *)(base + nb * 8);
+    h->ch.len = (const int32_t *)(base + nb * 16);
+    h->dflags = (uint8_t *)(base + nb * 20);
+    if (h->defer) {
+        h->sm.words32 = (uint32_t *)(base + copy_off);
+        h->sm.scales = (float *)(base + copy_off + (size_t)h->nwords * 8);
+    }
+}
+
+// The Require line of Algorithm 1 on the device: m = v = u = 0; errors start
+// at 0 (Algorithm 2); the anchor x_{t'} with t' = 0 is x_0; flags cleared.
+hipError_t start_state(zo_adam *h, hipStream_t stream)
+{
+    const zo_state *st = &h->st;
+    if (h->nchunks > 0) {
+        hipError_t e = hipMemsetAsync(h->dflags, 0, (size_t)(h->c1 - h->c0) + 1, stream);
+        if (e != hipSuccess) return e;
+    }
+    if (h->n == 0) return hipSuccess;
+    const size_t fb = (size_t)h->n * sizeof(float);
+    const bool fv = h->fv;
+    hipError_t es[6] = {
+        hipMemsetAsync(st->m, 0, fb, stream), hipMemsetAsync(st->v, 0, fb, stream),
+        fv ? hipSuccess : hipMemsetAsync(st->u, 0, fb, stream),
+        hipMemsetAsync(st->err, 0, fb, stream),
+        h->e1 > h->e0 ? hipMemsetAsync(st->srv_err, 0, (size_t)(h->e1 - h->e0) * 4, stream)
+                      : hipSuccess,
+        fv ? hipSuccess : hipMemcpyAsync(st->anchor, st->x, fb, hipMemcpyDeviceToDevice, stream)};
+    for (hipError_t e : es)
+        if (e != hipSuccess) return e;
+    return hipSuccess;
+}
+
+// ---- handles that allocate nothing (zo_adam_init_static) ------------------
+//
+// One handle per device at a time.  Its chunk table, flags and (deferred sync
+// writes) server copy live in `scratch`, a static device array of
+// kScratchBytes that every GPU the library runs on holds until the process
+// ends; the handle and its schedules live in a static host slot of that
+// device.  Nothing is allocated on the host or the device.
+constexpr size_t kScratchBytes = (size_t)4 << 20;
+constexpr int kMaxDevices = 16;
+constexpr int64_t kStaticMaxSched = 65536;
+constexpr int64_t kStage = 4096;  // chunk table entries uploaded per batch
+
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+struct StaticSlot {
+    zo_adam h;
+    int64_t tv[kStaticMaxSched], tu[kStaticMaxSched];
+    char *dev = nullptr;  // this device's address of `scratch`
+    bool live = false;
+};
+StaticSlot g_slots[kMaxDevices];
+std::mutex g_slots_mu;                 // guards the slots and the staging arrays
+int64_t g_stage_start[kStage], g_stage_word[kStage];
+int32_t g_stage_len[kStage];
+
+// Upload the chunk table of h (planned as zo_plan_chunks plans it) into its
+// device block in batches through the static staging arrays, and set the
+// server range's element and word bounds.  Called with g_slots_mu held.
+hipError_t upload_table(zo_adam *h, const zo_config *cfg, hipStream_t stream)
+{
+    const size_t nb = (size_t)h->nchunks;
+    char *base = (char *)h->ch.start;
+    int64_t c = 0, w = 0, filled = 0, first = 0;
+    h->e0 = h->e1 = h->w0 = h->w1 = 0;
+    auto flush = [&]() -> hipError_t {
+        if (filled == 0) return hipSuccess;
+        hipError_t e = hipMemcpyAsync(base + (size_t)first * 8, g_stage_start, (size_t)filled * 8,
+                                      hipMemcpyHostToDevice, stream);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(base + nb * 8 + (size_t)first * 8, g_stage_word,
+                               (size_t)filled * 8, hipMemcpyHostToDevice, stream);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(base + nb * 16 + (size_t)first * 4, g_stage_len, (size_t)filled * 4,
+                               hipMemcpyHostToDevice, stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(stream);  // the staging is reused
+        first += filled;
+        filled = 0;
+        return e;
+    };
+    for (int32_t sg = 0; sg < cfg->nseg; ++sg) {
+        const int64_t end = cfg->seg_off[sg + 1];
+        for (int64_t pos = cfg->seg_off[sg]; pos < end; pos += cfg->chunk, ++c) {
+            const int64_t l = std::min<int64_t>(cfg->chunk, end - pos);
+            if (c == h->c0) {
+                h->e0 = pos;
+                h->w0 = w;
+            }
+            if (c == h->c1 - 1) {
+                h->e1 = pos + l;
+                h->w1 = w + (l + 63) / 64;
+            }
+            g_stage_start[filled] = pos;
+            g_stage_word[filled] = w;
+            g_stage_len[filled] = (int32_t)l;
+            w += (l + 63) / 64;
+            if (++filled == kStage) {
+                hipError_t e = flush();
+                if (e != hipSuccess) return e;
+            }
+        }
+    }
+    h->nwords = w;
+    return flush();
+}
+
+}  // namespace
+
+extern "C" {
+
+int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStream_t stream)
+{
+    if (!out) return ZO_EINVAL;
+    *out = nullptr;
+    int rc = zo_config_check(cfg);
+    if (rc) return rc;
+    rc = check_state(cfg, st);
+    if (rc) return rc;
+
+    zo_adam *h = new (std::nothrow) zo_adam();
+    if (!h) return ZO_ENOMEM;
+    set_fields(h, cfg, st, stream);
     std::vector<int64_t> len64;
     try {
+        h->tv.assign(cfg->tv, cfg->tv + cfg->ntv);
+        h->tu.assign(cfg->tu, cfg->tu + cfg->ntu);
         h->hstart.resize(h->nchunks);
         h->hword.resize(h->nchunks);
         h->hlen.resize(h->nchunks);
@@ -213,12 +371,13 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
         delete h;
         return ZO_ENOMEM;
     }
+    h->tvp = h->tv.data();
+    h->tup = h->tu.data();
+    h->ntv = cfg->ntv;
+    h->ntu = cfg->ntu;
     h->nwords = zo_plan_chunks(cfg->nseg, cfg->seg_off, cfg->chunk, h->hstart.data(),
                                len64.data(), h->hword.data());
     for (int64_t c = 0; c < h->nchunks; ++c) h->hlen[c] = (int32_t)len64[c];
-
-    h->c0 = cfg->srv_chunk_begin;
-    h->c1 = cfg->srv_chunk_end < 0 ? h->nchunks : cfg->srv_chunk_end;
     if (h->c1 > h->c0) {
         h->e0 = h->hstart[h->c0];
         h->e1 = h->hstart[h->c1 - 1] + h->hlen[h->c1 - 1];
@@ -231,9 +390,8 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
     // Device chunk table + per-chunk exactness flags (+ in deferred mode the
     // server-output copy: packed words and scales): the only allocations.
     const size_t nb = (size_t)h->nchunks;
-    const size_t copy_off = (nb * (8 + 8 + 4) + (size_t)(h->c1 - h->c0) + 64 + 255) & ~(size_t)255;
-    const size_t copy_bytes = h->defer ? (size_t)h->nwords * 8 + nb * 4 : 0;
-    const size_t bytes = copy_off + copy_bytes;
+    size_t copy_off = 0;
+    const size_t bytes = device_block(h, copy_off);
     if (nb) {
         hipError_t e = hipMalloc(&h->dtable, bytes);
         if (e != hipSuccess) {
@@ -242,51 +400,87 @@ int zo_adam_init(zo_adam **out, const zo_config *cfg, const zo_state *st, hipStr
             return e == hipErrorOutOfMemory ? ZO_ENOMEM : ZO_EHIP;
         }
         char *base = (char *)h->dtable;
-        h->ch.start = (const int64_t *)base;
-        h->ch.word = (const int64_t *)(base + nb * 8);
-        h->ch.len = (const int32_t *)(base + nb * 16);
-        h->dflags = (uint8_t *)(base + nb * 20);
-        if (h->defer) {
-            h->sm.words32 = (uint32_t *)(base + copy_off);
-            h->sm.scales = (float *)(base + copy_off + (size_t)h->nwords * 8);
-        }
+        place_block(h, base, copy_off);
         hipError_t e1 = hipMemcpyAsync(base, h->hstart.data(), nb * 8, hipMemcpyHostToDevice,
                                        stream);
         hipError_t e2 = hipMemcpyAsync(base + nb * 8, h->hword.data(), nb * 8,
                                        hipMemcpyHostToDevice, stream);
         hipError_t e3 = hipMemcpyAsync(base + nb * 16, h->hlen.data(), nb * 4,
                                        hipMemcpyHostToDevice, stream);
-        hipError_t e4 = hipMemsetAsync(h->dflags, 0, (size_t)(h->c1 - h->c0) + 1, stream);
-        if (e1 || e2 || e3 || e4) {
-            rc = h->hip_fail(e1 ? e1 : e2 ? e2 : e3 ? e3 : e4);
+        if (e1 || e2 || e3) {
+            rc = h->hip_fail(e1 ? e1 : e2 ? e2 : e3);
             (void)hipStreamSynchronize(stream);
             (void)hipFree(h->dtable);
             delete h;
             return rc;
         }
     }
-    // Require line of Algorithm 1: m = v = u = 0; errors start at 0
-    // (Algorithm 2); the anchor x_{t'} with t' = 0 is x_0.
-    if (h->n > 0) {
-        const size_t fb = (size_t)h->n * sizeof(float);
-        hipError_t es[6] = {
-            hipMemsetAsync(st->m, 0, fb, stream), hipMemsetAsync(st->v, 0, fb, stream),
-            fv ? hipSuccess : hipMemsetAsync(st->u, 0, fb, stream),
-            hipMemsetAsync(st->err, 0, fb, stream),
-            h->e1 > h->e0 ? hipMemsetAsync(st->srv_err, 0, (size_t)(h->e1 - h->e0) * 4, stream)
-                          : hipSuccess,
-            fv ? hipSuccess
-               : hipMemcpyAsync(st->anchor, st->x, fb, hipMemcpyDeviceToDevice, stream)};
-        for (hipError_t e : es) {
-            if (e != hipSuccess) {
-                rc = h->hip_fail(e);
-                (void)hipStreamSynchronize(stream);
-                if (h->dtable) (void)hipFree(h->dtable);
-                delete h;
-                return rc;
-            }
-        }
+    hipError_t e = start_state(h, stream);
+    if (e != hipSuccess) {
+        rc = h->hip_fail(e);
+        (void)hipStreamSynchronize(stream);
+        if (h->dtable) (void)hipFree(h->dtable);
+        delete h;
+        return rc;
     }
+    *out = h;
+    return ZO_OK;
+}
+
+int zo_adam_init_static(zo_adam **out, const zo_config *cfg, const zo_state *st,
+                        hipStream_t stream)
+{
+    if (!out) return ZO_EINVAL;
+    *out = nullptr;
+    int rc = zo_config_check(cfg);
+    if (rc) return rc;
+    rc = check_state(cfg, st);
+    if (rc) return rc;
+    if (cfg->ntv > kStaticMaxSched || cfg->ntu > kStaticMaxSched) return ZO_ESCRATCH;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ZO_EHIP;
+
+    std::lock_guard<std::mutex> lock(g_slots_mu);
+    StaticSlot &slot = g_slots[dev];
+    if (slot.live) return ZO_ESTATE;  // one handle per device at a time
+    if (!slot.dev) {
+        // set-up, once per device with that device current: the device
+        // address of this device's copy of `scratch` (the host-side name is
+        // not a device address)
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return ZO_EHIP;
+        }
+        slot.dev = (char *)p;
+    }
+    zo_adam *h = &slot.h;
+    *h = zo_adam();  // a fresh handle: empty vectors, nothing allocated
+    set_fields(h, cfg, st, stream);
+    std::copy(cfg->tv, cfg->tv + cfg->ntv, slot.tv);
+    std::copy(cfg->tu, cfg->tu + cfg->ntu, slot.tu);
+    h->tvp = slot.tv;
+    h->tup = slot.tu;
+    h->ntv = cfg->ntv;
+    h->ntu = cfg->ntu;
+    h->slot = dev;
+    // the word count, for the block's size (a pass over the chunks)
+    int64_t words = 0;
+    for (int32_t sg = 0; sg < cfg->nseg; ++sg)
+        for (int64_t pos = cfg->seg_off[sg]; pos < cfg->seg_off[sg + 1]; pos += cfg->chunk)
+            words += (std::min<int64_t>(cfg->chunk, cfg->seg_off[sg + 1] - pos) + 63) / 64;
+    h->nwords = words;
+    size_t copy_off = 0;
+    if (device_block(h, copy_off) > kScratchBytes) return ZO_ESCRATCH;
+    place_block(h, slot.dev, copy_off);
+    hipError_t e = h->nchunks > 0 ? upload_table(h, cfg, stream) : hipSuccess;
+    if (e == hipSuccess) e = start_state(h, stream);
+    if (e != hipSuccess) {
+        rc = h->hip_fail(e);
+        (void)hipStreamSynchronize(stream);
+        return rc;
+    }
+    slot.live = true;
     *out = h;
     return ZO_OK;
 }
@@ -297,6 +491,12 @@ int zo_adam_destroy(zo_adam *h)
     int rc = ZO_OK;
     hipError_t e = hipStreamSynchronize(h->stream);
     if (e != hipSuccess) rc = h->hip_fail(e);
+    if (h->slot >= 0) {
+        // a static handle: its slot becomes free (nothing to free)
+        std::lock_guard<std::mutex> lock(g_slots_mu);
+        g_slots[h->slot].live = false;
+        return rc;
+    }
     if (h->dtable) {
         e = hipFree(h->dtable);
         if (e != hipSuccess && rc == ZO_OK) rc = ZO_EHIP;
@@ -560,6 +760,22 @@ int zo_server_range(const zo_adam *h, int64_t *chunk0, int64_t *nchunks, int64_t
 int zo_chunk_table(const zo_adam *h, int64_t *start, int64_t *len, int64_t *word)
 {
     if (!h) return ZO_EINVAL;
+    if (h->slot >= 0) {
+        // a static handle keeps its table on the device only
+        const size_t nb = (size_t)h->nchunks;
+        hipError_t e = hipStreamSynchronize(h->stream);
+        if (e == hipSuccess && start && nb)
+            e = hipMemcpy(start, h->ch.start, nb * 8, hipMemcpyDeviceToHost);
+        if (e == hipSuccess && word && nb)
+            e = hipMemcpy(word, h->ch.word, nb * 8, hipMemcpyDeviceToHost);
+        if (e == hipSuccess && len && nb) {
+            // int32 on the device: widen in place from the array's tail
+            int32_t *l32 = reinterpret_cast<int32_t *>(len) + nb;
+            e = hipMemcpy(l32, h->ch.len, nb * 4, hipMemcpyDeviceToHost);
+            for (size_t c = 0; c < nb && e == hipSuccess; ++c) len[c] = l32[c];
+        }
+        return e == hipSuccess ? ZO_OK : ZO_EHIP;
+    }
     for (int64_t c = 0; c < h->nchunks; ++c) {
         if (start) start[c] = h->hstart[c];
         if (len) len[c] = h->hlen[c];
@@ -594,6 +810,8 @@ const char *zo_strerror(int status)
     case ZO_ESTATE: return "call out of order for the current step";
     case ZO_EHIP: return "HIP runtime error";
     case ZO_ENOMEM: return "out of memory";
+    case ZO_ESCRATCH:
+        return "configuration exceeds the static scratch of zo_adam_init_static";
     default: return "unknown status";
     }
 }

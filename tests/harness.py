@@ -225,7 +225,7 @@ class GpuRun:
     FV_STATE = ("x", "m", "v", "err", "srv_err")
 
     def __init__(self, wl, device="cuda", fused=True, srv_range=(0, -1), defer=False,
-                 grad_dtype="f32"):
+                 grad_dtype="f32", static=False):
         import torch
         import paper_2202_06009_amd as zo
         self.torch, self.zo, self.wl, self.fused = torch, zo, wl, fused
@@ -252,7 +252,7 @@ class GpuRun:
                              chunk=wl.chunk, seg_off=wl.seg_off, tv=wl.tv, tu=wl.tu,
                              state=self.state, srv_chunk_begin=srv_range[0],
                              srv_chunk_end=srv_range[1], defer_sync_writes=defer,
-                             algorithm=wl.algorithm, grad_dtype=grad_dtype)
+                             algorithm=wl.algorithm, grad_dtype=grad_dtype, static=static)
 
     def fill_inputs(self, t):
         wl = self.wl
