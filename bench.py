@@ -36,7 +36,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2202_06009_amd", "csrc", "zo_kernels.hip")
+# the device code of the library: the traffic summary is valid for these sources only
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2202_06009_amd", "csrc", f)
+                  for f in ("zo_device.h", "zo_kernels.hip", "zo_server.hip", "zo_kernels_ua.hip")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gpt2-1.5b_hbm_traffic.json")
 COPY_BYTES = 4 << 30          # size of the calibration copies
 # kernel-name prefixes in rocprofv3 output -> bench names; every hot kernel
@@ -70,8 +72,11 @@ def kernel_keys(mode):
 
 
 def source_hash():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def summarize_counters(dirs, mode):
