@@ -301,32 +301,103 @@ __device__ __forceinline__ void m_from_copy_body(float *__restrict__ m, const Ch
 // chunk machinery
 // ---------------------------------------------------------------------------
 
-// Sum over the lanes of a chunk that share a wave: xor butterfly.
-template <int L>
-__device__ __forceinline__ float wave_tree(float x)
+// One level of an xor butterfly across the lanes of a wave: both lanes of
+// each pair (i, i ^ H) get op(value of the lower lane, value of the upper).
+// The pairs are formed by lane permutations in the vector ALU (DPP inside
+// 16-lane rows; the row-swap instructions across rows), not through the LDS.
+// Every lane of the wave must be active.
+template <int H, class Op>
+__device__ __forceinline__ uint32_t butterfly(uint32_t x, Op op)
 {
-#pragma unroll
-    for (int o = 1; o < (L < 64 ? L : 64); o <<= 1) x = x + __shfl_xor(x, o);
+    static_assert(H == 1 || H == 2 || H == 4 || H == 8 || H == 16 || H == 32, "lane offset");
+    const int v = (int)x;
+    if constexpr (H <= 8) {
+        // DPP controls: quad_perm [1,0,3,2] = i^1, [2,3,0,1] = i^2,
+        // [3,2,1,0] = i^3; row_mirror = i^15 and row_half_mirror = i^7 in a row
+        int y;
+        if constexpr (H == 1) {
+            y = __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);
+        } else if constexpr (H == 2) {
+            y = __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);
+        } else if constexpr (H == 4) {  // i^3, then ^7
+            y = __builtin_amdgcn_mov_dpp(__builtin_amdgcn_mov_dpp(v, 0x1B, 0xF, 0xF, false), 0x141,
+                                         0xF, 0xF, false);
+        } else {  // i^15, then ^7
+            y = __builtin_amdgcn_mov_dpp(__builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, false), 0x141,
+                                         0xF, 0xF, false);
+        }
+        const uint32_t o = (uint32_t)y;
+        return (threadIdx.x & H) ? op(o, x) : op(x, o);
+    } else {
+        // the swap returns {lower row or half in every lane, upper in every lane}
+        const auto r = H == 16 ? __builtin_amdgcn_permlane16_swap(x, x, false, false)
+                               : __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        return op((uint32_t)r[0], (uint32_t)r[1]);
+    }
+}
+
+// op over aligned groups of N lanes (N a power of two, at most 64), the
+// result in every lane of the group: the butterfly levels 1, 2, .., N/2.
+template <int N, class Op>
+__device__ __forceinline__ uint32_t lanes_reduce(uint32_t x, Op op)
+{
+    static_assert(N >= 1 && N <= 64 && (N & (N - 1)) == 0, "group size");
+    if constexpr (N > 1) x = butterfly<1>(x, op);
+    if constexpr (N > 2) x = butterfly<2>(x, op);
+    if constexpr (N > 4) x = butterfly<4>(x, op);
+    if constexpr (N > 8) x = butterfly<8>(x, op);
+    if constexpr (N > 16) x = butterfly<16>(x, op);
+    if constexpr (N > 32) x = butterfly<32>(x, op);
     return x;
 }
 
-template <int L>
+// The cross-lane steps of the chunk machinery come in two forms.  DPP: lane
+// permutations in the vector ALU (butterfly above), used by the server's
+// compression.  Otherwise LDS-routed shuffles (__shfl_xor), used by the
+// worker's compress kernel: there they measured faster, although the LDS
+// form holds more registers.  Both add the same pairs in the same order.
+
+// Sum over the lanes of a chunk that share a wave: an xor butterfly with
+// rising offsets (the index-order pairwise tree over those lanes).
+template <int L, bool DPP>
+__device__ __forceinline__ float wave_tree(float x)
+{
+    constexpr int N = L < 64 ? L : 64;
+    if constexpr (!DPP) {
+#pragma unroll
+        for (int o = 1; o < N; o <<= 1) x = x + __shfl_xor(x, o);
+        return x;
+    } else {
+        const auto add = [](uint32_t a, uint32_t b) {
+            return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+        };
+        return __uint_as_float(lanes_reduce<N>(__float_as_uint(x), add));
+    }
+}
+
+// OR over aligned groups of 8 lanes (fewer when L < 8).
+template <int L, bool DPP>
 __device__ __forceinline__ uint32_t wave_or8(uint32_t x)
 {
+    constexpr int N = L < 8 ? L : 8;
+    if constexpr (!DPP) {
 #pragma unroll
-    for (int o = 1; o < (L < 8 ? L : 8); o <<= 1) x |= (uint32_t)__shfl_xor((int)x, o);
-    return x;
+        for (int o = 1; o < N; o <<= 1) x |= (uint32_t)__shfl_xor((int)x, o);
+        return x;
+    } else {
+        return lanes_reduce<N>(x, [](uint32_t a, uint32_t b) { return a | b; });
+    }
 }
 
 // The chunk's pairwise L1 tree from each lane's per-block partial sums (the
 // in-lane level).  Returns the total to every lane of the chunk.  Every
 // thread of the workgroup must call it (it synchronises when L > 64).  `lds`
 // holds (blockDim / 64) * V floats.
-template <int L, int V>
+template <int L, int V, bool DPP>
 __device__ __forceinline__ float chunk_tree(float (&part)[V], float *lds)
 {
 #pragma unroll
-    for (int k = 0; k < V; ++k) part[k] = wave_tree<L>(part[k]);
+    for (int k = 0; k < V; ++k) part[k] = wave_tree<L, DPP>(part[k]);
     if constexpr (L <= 64) {
         // the chunk's lanes share a wave: the in-order tree over its blocks
 #pragma unroll
@@ -335,7 +406,25 @@ __device__ __forceinline__ float chunk_tree(float (&part)[V], float *lds)
             for (int k = 0; k + h < V; k += 2 * h) part[k] = part[k] + part[k + h];
         }
         return part[0];
+    } else if constexpr (DPP) {
+        // The wave totals of block k sit at k * NW + w (w: the chunk's wave),
+        // at most 64 of them.  Lane j of every wave takes the one at j mod NP,
+        // and the butterfly with rising offsets forms the tree over w (the low
+        // index bits), then over k: one value per lane.
+        constexpr int NW = L / 64;  // waves per chunk
+        constexpr int NP = NW * V;  // wave totals per chunk
+        static_assert(NP <= 64, "one wave holds the chunk's wave totals");
+        const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+        const int base = (wave / NW) * NP;
+        __syncthreads();  // lds may still be read by a previous call
+        if (lane == 0) {
+#pragma unroll
+            for (int k = 0; k < V; ++k) lds[base + k * NW + wave % NW] = part[k];
+        }
+        __syncthreads();
+        return wave_tree<NP, true>(lds[base + (lane & (NP - 1))]);
     } else {
+        // every lane reads the chunk's NW * V wave totals and forms the tree
         constexpr int NW = L / 64;  // waves per chunk
         const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
         __syncthreads();  // lds may still be read by a previous call
@@ -389,8 +478,9 @@ __device__ __forceinline__ float ef_elem(float a, float s)
 // AL: the chunk's elements start on a 16-byte boundary and len is a multiple
 // of 4 (see At4 / At1).
 // get_a(k) returns block k of a (from registers or from where the caller
-// stashed it); part[k] = abs4 of it, formed by the caller.
-template <int L, int V, bool AL, class GetA>
+// stashed it); part[k] = abs4 of it, formed by the caller.  DPP: the form of
+// the cross-lane steps (see wave_tree).
+template <int L, int V, bool AL, bool DPP, class GetA>
 __device__ __forceinline__ void compress_chunk_from(const float (&part_in)[V], GetA get_a, int lc,
                                                     int len, bool active,
                                                     float *__restrict__ err, int64_t err_e0,
@@ -400,7 +490,7 @@ __device__ __forceinline__ void compress_chunk_from(const float (&part_in)[V], G
     float part[V];
 #pragma unroll
     for (int k = 0; k < V; ++k) part[k] = part_in[k];
-    const float tot = chunk_tree<L, V>(part, lds);
+    const float tot = chunk_tree<L, V, DPP>(part, lds);
     const float s = tot / (float)len;
     const int ndw = 2 * ((len + 63) >> 6);
     uint32_t pend = 0;  // L < 8: several blocks share a dword
@@ -418,7 +508,7 @@ __device__ __forceinline__ void compress_chunk_from(const float (&part_in)[V], G
             st(err, a, d);
             nib = inside_bits(sign4(ak), a);
         }
-        const uint32_t dw = wave_or8<L>(nib << (4 * (lc & 7)));
+        const uint32_t dw = wave_or8<L, DPP>(nib << (4 * (lc & 7)));
         if constexpr (L >= 8) {
             // lanes 8q..8q+7 hold dword 4Lk/32 + q
             if (active && (lc & 7) == 0) {
@@ -440,6 +530,7 @@ __device__ __forceinline__ void compress_chunk_from(const float (&part_in)[V], G
     if (active && lc == 0) *scale_out = s;
 }
 
+// The server's compression of its average plus error, held in registers.
 template <int L, int V, bool AL>
 __device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, bool active,
                                                float *__restrict__ err, int64_t err_e0,
@@ -449,8 +540,8 @@ __device__ __forceinline__ void compress_chunk(f4v (&a)[V], int lc, int len, boo
     float part[V];
 #pragma unroll
     for (int k = 0; k < V; ++k) part[k] = abs4(a[k]);
-    compress_chunk_from<L, V, AL>(part, [&](int k) { return a[k]; }, lc, len, active, err,
-                                  err_e0, words32, scale_out, lds);
+    compress_chunk_from<L, V, AL, true>(part, [&](int k) { return a[k]; }, lc, len, active, err,
+                                        err_e0, words32, scale_out, lds);
 }
 
 
@@ -509,7 +600,7 @@ __device__ __forceinline__ void sync1_body(const void *__restrict__ g, const flo
         else
             a[k] = ak;
     }
-    compress_chunk_from<L, V, AL>(
+    compress_chunk_from<L, V, AL, false>(
         part, [&](int k) { return kStash ? stash[k * L + lc] : a[kStash ? 0 : k]; }, lc, len,
         active, err, e0, packed32 + 2 * (active ? ch.word[c] : 0), scales + (active ? c : 0), lds);
 }

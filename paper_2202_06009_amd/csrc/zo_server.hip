@@ -40,12 +40,13 @@ __device__ __forceinline__ uint32_t inexact_flag(const float *__restrict__ sc, i
             hi = max(hi, h);
         }
     }
-#pragma unroll
-    for (int o = 1; o < LW; o <<= 1) {
-        lo = min(lo, __shfl_xor(lo, o));
-        hi = max(hi, __shfl_xor(hi, o));
-        bad |= __shfl_xor(bad, o);
-    }
+    lo = (int)lanes_reduce<LW>((uint32_t)lo, [](uint32_t a, uint32_t b) {
+        return (uint32_t)min((int)a, (int)b);
+    });
+    hi = (int)lanes_reduce<LW>((uint32_t)hi, [](uint32_t a, uint32_t b) {
+        return (uint32_t)max((int)a, (int)b);
+    });
+    bad = (int)lanes_reduce<LW>((uint32_t)bad, [](uint32_t a, uint32_t b) { return a | b; });
     int lg = 0;
     while ((1 << lg) < W) ++lg;
     if (hi < lo) return (uint32_t)bad;  // every scale is zero
