@@ -79,12 +79,23 @@ def source_hash():
     return h.hexdigest()
 
 
+# Reference kernels of a counter run (--copy-calibration): the calibration
+# copy and the stream mixes, plain streams of R read and S write arrays.
+REFERENCE_KERNELS = {r"zo::k_copy<true>": "copy", r"zo::k_stream<1, 1>": "1r+1w",
+                     r"zo::k_stream<3, 1>": "3r+1w", r"zo::k_stream<3, 2>": "3r+2w",
+                     r"zo::k_stream<4, 3>": "4r+3w"}
+
+
 def summarize_counters(dirs, mode):
     """Mean per dispatch of every counter in the rocprofv3 --pmc runs under
-    `dirs`, for each timed kernel of `mode`, as a markdown table, with the
-    ratios that need no unit: instructions per wave, and the share of the
-    LDS's active cycles lost to bank conflicts."""
-    keys = kernel_keys(mode)
+    `dirs`, for each timed kernel of `mode` and each reference kernel present,
+    as a markdown table, with the ratios that need no unit: instructions per
+    wave, the share of the LDS's active cycles lost to bank conflicts, the
+    average latency of the L2's memory requests (requests in flight summed
+    over cycles, over requests) and the share of L2 cycles stalled for
+    memory credits."""
+    keys = {p: k for p, (k, kind) in kernel_keys(mode).items() if kind is not None}
+    keys.update(REFERENCE_KERNELS)
     vals = {}
     for d in dirs:
         for root, _, files in os.walk(d):
@@ -93,11 +104,11 @@ def summarize_counters(dirs, mode):
                     continue
                 for r in csv.DictReader(open(os.path.join(root, fn))):
                     name = r["Kernel_Name"].replace("void ", "")
-                    for pattern, (key, kind) in keys.items():
-                        if kind is not None and re.match(pattern, name):
+                    for pattern, key in keys.items():
+                        if re.match(pattern, name):
                             vals.setdefault(key, {}).setdefault(r["Counter_Name"], []).append(
                                 float(r["Counter_Value"]))
-    names = [k for _, (k, kind) in keys.items() if kind is not None and k in vals]
+    names = [k for k in keys.values() if k in vals]
     mean = {k: {c: sum(v) / len(v) for c, v in vals[k].items()} for k in names}
     counters = sorted({c for k in names for c in mean[k]})
     print("| counter | " + " | ".join(names) + " |")
@@ -112,8 +123,24 @@ def summarize_counters(dirs, mode):
                         ("SALU instructions per wave", "SQ_INSTS_SALU", "SQ_WAVES"),
                         ("vector memory reads per wave", "SQ_INSTS_VMEM_RD", "SQ_WAVES"),
                         ("LDS bank-conflict cycles / LDS active cycles", "SQ_LDS_BANK_CONFLICT",
-                         "SQ_LDS_IDX_ACTIVE")):
-        print(f"| {label} | " + " | ".join(ratio(k, a, b) for k in names) + " |")
+                         "SQ_LDS_IDX_ACTIVE"),
+                        ("memory reads in flight per L2 channel", "TCC_EA0_RDREQ_LEVEL",
+                         "TCC_CYCLE"),
+                        ("memory writes in flight per L2 channel", "TCC_EA0_WRREQ_LEVEL",
+                         "TCC_CYCLE"),
+                        ("memory read latency (L2 cycles)", "TCC_EA0_RDREQ_LEVEL", "TCC_EA0_RDREQ"),
+                        ("memory write latency (L2 cycles)", "TCC_EA0_WRREQ_LEVEL",
+                         "TCC_EA0_WRREQ"),
+                        ("L2 cycles with a read stalled for DRAM credits",
+                         "TCC_EA0_RDREQ_DRAM_CREDIT_STALL", "TCC_CYCLE"),
+                        ("L2 cycles with a write stalled for DRAM credits",
+                         "TCC_EA0_WRREQ_DRAM_CREDIT_STALL", "TCC_CYCLE"),
+                        ("L2 cycles with a write request stalled", "TCC_EA0_WRREQ_STALL",
+                         "TCC_CYCLE"),
+                        ("L2 cycles with a request pending", "TCC_BUSY", "TCC_CYCLE")):
+        row = [ratio(k, a, b) for k in names]
+        if any(r != "-" for r in row):
+            print(f"| {label} | " + " | ".join(row) + " |")
 
 
 def trace_rows(trace_dir):
@@ -991,10 +1018,16 @@ def main():
     props = torch.cuda.get_device_properties(dev)
     # Measurements after the timed region.  A counter-collection run
     # (--copy-calibration) skips them: its counters must come from the timed
-    # kernels and the calibration copies only (the server share and the
-    # schedule run launch the same kernels at other sizes, the ceiling the
-    # same copy kernel).
+    # kernels, the calibration copies and the reference streams only (the
+    # server share and the schedule run launch the same kernels at other
+    # sizes, the ceiling the same copy kernel).
     extras = not args.copy_calibration
+    if args.copy_calibration and args.grad_dtype == "f32":
+        # reference streams for the counters: each kernel's mix, and one read
+        # and one write array
+        stream_mix_ceilings(zo, torch, state, g, gb, d, mode)
+        zo.zo_diag_stream([g], [state["x"]])
+        torch.cuda.synchronize()
     share = sched = mix = pattern = graphed = general = None
     copy_gbs = float("nan")
     if extras and not fv:

@@ -130,3 +130,35 @@ def test_kernel_names_map_to_variants():
                 assert bench.variant_of_kernel(k) == (name + ("+var" if var else ""),
                                                       4 if name == "srv" else gb), k
     assert bench.variant_of_kernel("zo::k_copy<true>") is None
+
+
+def test_counter_summary_ratios(tmp_path, capsys):
+    """The counter summary averages each counter per dispatch for the step's
+    kernels and the reference kernels, and forms the unit-free ratios: reads
+    in flight per channel and read latency from the request-level sums."""
+    cols = ["Kernel_Name", "Counter_Name", "Counter_Value"]
+    rows = []
+    for rep in range(2):  # two dispatches of each kernel: the mean is taken
+        for name, level, req, cyc in (("zo::k_local<true, 1, false, 0>", 600.0, 2.0, 3.0),
+                                      ("zo::k_copy<true>", 100.0 + 20 * rep, 0.5, 1.0),
+                                      ("zo::k_stream<4, 3>", 300.0, 1.0, 1.5)):
+            rows += [(f"void {name}(int)", "TCC_EA0_RDREQ_LEVEL", level),
+                     (f"void {name}(int)", "TCC_EA0_RDREQ", req),
+                     (f"void {name}(int)", "TCC_CYCLE", cyc)]
+    d = tmp_path / "pmc"
+    d.mkdir()
+    with open(d / "run_counter_collection.csv", "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(cols)
+        w.writerows(rows)
+    bench.summarize_counters([str(d)], "deferred")
+    out = capsys.readouterr().out.splitlines()
+    assert out[0] == "| counter | local+var | copy | 4r+3w |"
+    table = {line.split("|")[1].strip(): [c.strip() for c in line.split("|")[2:-1]]
+             for line in out[2:]}
+    assert table["TCC_EA0_RDREQ_LEVEL"] == ["600", "110", "300"]
+    assert table["memory read latency (L2 cycles)"] == ["300", "220", "300"]
+    assert table["memory reads in flight per L2 channel"] == ["200", "110", "200"]
+    # rows whose counters were not taken are left out
+    assert "L2 cycles with a request pending" not in table
+    assert "LDS instructions per wave" not in table
