@@ -280,7 +280,7 @@ constexpr int kMaxDevices = 16;
 constexpr int64_t kStaticMaxSched = 65536;
 constexpr int64_t kStage = 4096;  // chunk table entries uploaded per batch
 
-__device__ __align__(256) uint8_t scratch[kScratchBytes];
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 
 struct StaticSlot {
     zo_adam h;
