@@ -71,6 +71,23 @@ def kernel_keys(mode):
             rf"zo::k_recon<true, {dv}, {gt}>": ("recon+var", "nt")} | copies
 
 
+def device_clocks(dev=0):
+    """Peak shader and memory clocks in MHz as the HIP runtime reports them
+    (hipDeviceGetAttribute: hipDeviceAttributeClockRate = 5 and
+    hipDeviceAttributeMemoryClockRate = 60, in kHz), or {} when unavailable."""
+    import ctypes
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+    except OSError:
+        return {}
+    out = {}
+    for key, attr in (("sclk_mhz", 5), ("mclk_mhz", 60)):
+        v = ctypes.c_int(0)
+        if hip.hipDeviceGetAttribute(ctypes.byref(v), ctypes.c_int(attr), ctypes.c_int(dev)) == 0:
+            out[key] = v.value / 1000.0
+    return out
+
+
 def source_hash():
     h = hashlib.sha256()
     for path in KERNEL_SOURCES:
@@ -1125,7 +1142,7 @@ def main():
             4),
         "env": {"device": props.name, "arch": getattr(props, "gcnArchName", None),
                 "compute_units": props.multi_processor_count, "hip": torch.version.hip,
-                "torch": torch.__version__},
+                "torch": torch.__version__, **device_clocks(dev.index or 0)},
         # each step of the path in its general form (every state read and written)
         "general_kernels": general,
         "roofline": {"bound": "hbm", "kernel": dom,
