@@ -420,6 +420,60 @@ def algorithmic_bytes(d, nchunks, nwords, W, deferred=True, gbytes=4):
     return {k: variant_bytes(name, d, nchunks, nwords, W, gbytes) for k, name in v.items()}
 
 
+def placement_study(zo, torch, d, reps=5):
+    """The plain stream kernel (zo_diag_stream) over the general local step's
+    arrays (reads g, m, x, v, u; rewrites m, x, u in place: 32 B/param) of
+    length d, timed (best of `reps` launches after one untimed) with the five
+    arrays placed in different ways: five separate allocations; one
+    allocation holding them back to back or 4 KiB or 2 MiB + 4 KiB apart; five
+    separate allocations after 48 GB of other allocations, or followed by
+    them.  Every layout's memory is returned to the driver before the next."""
+    gbytes = 32.0 * d / 1e9
+    f32 = dict(dtype=torch.float32, device="cuda")
+    dummy_n = 12 * 10 ** 9  # 48 GB of binary32
+
+    def timed(arrs):
+        g, m, x, v, u = arrs
+        best = None
+        for r in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            zo.zo_diag_stream([g, m, x, v, u], [m, x, u])
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            if r and (best is None or ms < best):
+                best = ms
+        return {"ms": round(best, 4), "gbs": round(gbytes / (best / 1000.0), 1),
+                "frac": round(gbytes / (best / 1000.0) / HBM_PEAK_GBS, 4)}
+
+    def separate():
+        return [torch.zeros(d, **f32) for _ in range(5)]
+
+    def slab(pad):
+        buf = torch.zeros(5 * (d + pad), **f32)
+        return [buf[i * (d + pad):i * (d + pad) + d] for i in range(5)]
+
+    out = {}
+    layouts = (("separate", lambda: (separate(), None)),
+               ("one allocation, back to back", lambda: (slab(0), None)),
+               ("one allocation, 4 KiB apart", lambda: (slab(1024), None)),
+               ("one allocation, 2 MiB + 4 KiB apart", lambda: (slab((2 << 20) // 4 + 1024), None)),
+               ("separate, after 48 GB of other allocations",
+                lambda: (lambda dm: (separate(), dm))(torch.empty(dummy_n, **f32))),
+               ("separate, followed by 48 GB of other allocations",
+                lambda: (lambda a: (a, torch.empty(dummy_n, **f32)))(separate())),
+               ("separate, again", lambda: (separate(), None)))
+    for name, make in layouts:
+        arrs, dummy = make()
+        out[name] = timed(arrs)
+        print(f"[bench] placement: {name}: {out[name]}", file=sys.stderr, flush=True)
+        del arrs, dummy
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return out
+
+
 def stream_mix_ceilings(zo, torch, state, g, gb, d, mode):
     """HBM rate of a plain streaming kernel (zo_diag_stream) with each hot
     kernel's mix of full-length arrays, on the bench's own buffers (used as
@@ -888,6 +942,9 @@ def main():
     ap.add_argument("--algorithm", choices=("zero-one", "frozen-variance"), default="zero-one",
                     help="frozen-variance: Algorithm 4 (1-bit Adam's compression stage), one "
                          "full-precision and one compressed step per bench step")
+    ap.add_argument("--placement-study", action="store_true",
+                    help="time the general local step's stream mix with its arrays placed in "
+                         "several ways (one JSON line), then exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="counter-collection run: first run plain and nontemporal copies of a "
                          "known size, and skip the measurements after the timed region")
@@ -929,7 +986,8 @@ def main():
     # the chunk-parallel oracle run forks, so it runs before anything here
     # initialises the GPU
     cpu_parallel = None
-    if not args.no_cpu_baseline and args.cpu_cores > 1 and not gpu_device_open():
+    if (not args.no_cpu_baseline and not args.placement_study and args.cpu_cores > 1
+            and not gpu_device_open()):
         print(f"[bench] timing the CPU oracle on {args.cpu_cores} cores", file=sys.stderr,
               flush=True)
         cpu_parallel = cpu_baseline_parallel(wl, args.cpu_sample_chunks, fv, args.cpu_cores)
@@ -939,6 +997,13 @@ def main():
     import synth
 
     zo.lib()
+    if args.placement_study:
+        res = placement_study(zo, torch, wl.n)
+        print(json.dumps({"placement_study": res, "workload": wl.name, "params": wl.n,
+                          "gb_per_launch": round(32.0 * wl.n / 1e9, 3),
+                          "env": {"device": torch.cuda.get_device_properties(0).name,
+                                  **device_clocks(0)}}))
+        return
     if args.copy_calibration:
         src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
