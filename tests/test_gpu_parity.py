@@ -121,6 +121,8 @@ SMALL = [
     ([20000, 16384, 4], 16384, 100),         # LD512 G13 at the GPT-2 chunk, the last of 4 workers
     ([6000, 2048, 2044], 2048, 20),          # LD64 G3, the last of 4 workers
     ([8192, 4096, 100], 4096, 72),           # LD128 G9
+    ([8192, 8192, 8000], 8192, 88),          # LD256 G11 (three waves per SIMD)
+    ([32768, 16384, 12], 16384, 120),        # LD512 G15 (three waves per SIMD)
     ([3000, 500, 12], 256, 128),             # half tables: LD8 G16
     ([700, 64, 36], 32, 64),                 # half tables: LD1 G8
     ([5000, 1000], 1024, 300),               # tables beyond the LDS budget: plain server
