@@ -1,7 +1,9 @@
 """zo_adam_init_static, the entry point for callers that cannot allocate,
 against zo_adam_init through the C ABI: two static handles in a row (the
 second on a smaller shard, reusing the static scratch the first left behind),
-each run step by step beside a handle from zo_adam_init on the same inputs;
+each run step by step beside a handle from zo_adam_init on the same inputs
+(the first with deferred sync writes, the second at a chunk length that is not
+a multiple of 4);
 every state, packed word and scale must be equal after every step (-0 == +0),
 and so must the chunk table read back from the device."""
 import numpy as np
@@ -60,7 +62,7 @@ def test_static_handle_equals_allocating_handle(torch_cuda):
     torch = torch_cuda
     first = _wl("static-first", [20000, 3000, 7000, 4], 1024, 8, 7, tu=[1, 2, 4, 6],
                 tv=[0, 1, 3])
-    second = _wl("static-second", [3000, 1000], 100, 4, 5, tu=[0, 2, 3], tv=[0, 4])
+    second = _wl("static-second", [3000, 1000], 99, 4, 5, tu=[0, 2, 3], tv=[0, 4])  # unaligned
     assert second.n < first.n
     _run_pair(torch, first, defer=True)
     _run_pair(torch, second, defer=False)
