@@ -185,17 +185,20 @@ def test_zero_gradient_segments(torch_cuda, defer):
         grun.close()
 
 
-def test_server_range_matches_single_server(torch_cuda):
+@pytest.mark.parametrize("chunk,world", [(1024, 8), (1021, 8), (4096, 128)],
+                         ids=["C1024-W8", "C1021-W8", "C4096-W128"])
+def test_server_range_matches_single_server(torch_cuda, chunk, world):
     """The server half restricted to a chunk range (one GPU's share in a
     sharded run) computes, on that range, exactly what the single server
-    computes there."""
+    computes there: the lookup-table server, the plain server at a chunk
+    length that is not a multiple of 4, and 16 worker groups."""
     import harness
     import paper_2202_06009_amd as zo
     torch = torch_cuda
-    wl = _wl(segs=(20000, 3000, 7000), chunk=1024, world=8, T=4, tu=(0, 1, 2, 3), tv=(0,))
+    wl = _wl(segs=(20000, 3000, 7000), chunk=chunk, world=world, T=4, tu=(0, 1, 2, 3), tv=(0,))
     full = harness.GpuRun(wl)
     _, ln, word, nw = zo.zo_plan_chunks(wl.seg_off, wl.chunk)
-    c0, c1 = 5, 17
+    c0, c1 = len(ln) // 4, 3 * len(ln) // 4 + 1  # an inner range, ragged chunks included
     part = harness.GpuRun(wl, srv_range=(c0, c1))
     try:
         rng_ = part.opt.server_range()
@@ -224,7 +227,7 @@ def test_server_range_matches_single_server(torch_cuda):
             part.srv_scales.copy_(full.srv_scales)
             part.opt.sync_update(t, part.srv_packed, part.srv_scales,
                                  part.gb if t in wl.tv else None)
-        assert W == 8
+        assert W == world
     finally:
         full.close()
         part.close()
