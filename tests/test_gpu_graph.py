@@ -3,7 +3,8 @@ kernel and allocates nothing, so a steady-state step pair (a local+variance
 step, then a sync+variance step with deferred writes) captured once replays
 as often as wanted.  Each replay is checked, bit for bit and over every
 buffer the path writes, against the same steps run eagerly on a twin handle
-in lockstep."""
+in lockstep.  The captured handle is also taken from zo_adam_init_static,
+whose device memory is the library's static array."""
 import numpy as np
 import pytest
 
@@ -25,14 +26,15 @@ def torch_cuda():
 class Twin:
     """One worker's handle with its own buffers, fed the inputs given."""
 
-    def __init__(self, torch, zo, seg, W, chunk, T, x0, g, gb, peers, peer_scales):
+    def __init__(self, torch, zo, seg, W, chunk, T, x0, g, gb, peers, peer_scales,
+                 static=False):
         d = seg[-1]
         self.state = {k: torch.zeros(d, dtype=torch.float32, device="cuda") for k in KEYS}
         self.state["x"].copy_(x0)
         self.g, self.gb = g.clone(), gb.clone()
         self.opt = zo.ZoAdam(beta1=0.9, beta2=0.999, eps=1e-8, world=W, chunk=chunk,
                              seg_off=seg, tv=list(range(T)), tu=list(range(1, T, 2)),
-                             state=self.state, defer_sync_writes=True)
+                             state=self.state, defer_sync_writes=True, static=static)
         self.packed = torch.zeros((W, self.opt.nwords), dtype=torch.int64, device="cuda")
         self.scales = torch.zeros((W, self.opt.nchunks), dtype=torch.float32, device="cuda")
         self.packed[1:] = peers
@@ -57,7 +59,8 @@ def _bits(t):
     return t.cpu().numpy().view(np.uint32 if t.element_size() == 4 else np.uint64)
 
 
-def test_captured_step_pair_replays_bit_exactly(torch_cuda):
+@pytest.mark.parametrize("static", [False, True], ids=["init", "init_static"])
+def test_captured_step_pair_replays_bit_exactly(torch_cuda, static):
     import paper_2202_06009_amd as zo
     torch = torch_cuda
     seg = C.offsets([5000, 3 * 2048 + 100, 12])
@@ -72,7 +75,7 @@ def test_captured_step_pair_replays_bit_exactly(torch_cuda):
     peers = torch.randint(-2**62, 2**62, (W - 1, nwords), device="cuda", generator=gen)
     peer_scales = 2.0e-8 * (1.0 + 0.5 * torch.rand((W - 1, nch), device="cuda", generator=gen))
     eager = Twin(torch, zo, seg, W, chunk, T, x0, g, gb, peers, peer_scales)
-    graphed = Twin(torch, zo, seg, W, chunk, T, x0, g, gb, peers, peer_scales)
+    graphed = Twin(torch, zo, seg, W, chunk, T, x0, g, gb, peers, peer_scales, static=static)
     try:
         # the first pair eagerly on both: it leaves the deferred-write state
         # (model in the anchor, buffer implicit) that every later pair starts from
